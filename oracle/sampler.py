@@ -49,12 +49,12 @@ def decision_values(z: np.ndarray, temperature: float) -> np.ndarray:
     return np.exp(y - y.max()).astype(np.float32)
 
 
-def kept_set(e: np.ndarray, top_p: float) -> tuple[np.ndarray, float]:
-    """Boolean mask of the nucleus and the top-p margin (relative to S)."""
+def _kept(e: np.ndarray, top_p: float):
+    """(nucleus mask, top-p margin relative to S, the kept set the nearest flip would give)."""
     e64 = e.astype(np.float64)
     total = e64.sum()
     if top_p >= 1.0:
-        return np.ones(e.size, dtype=bool), np.inf
+        return np.ones(e.size, dtype=bool), np.inf, None
     order = np.lexsort((np.arange(e.size), -e64))  # e descending, then id ascending
     cum = np.cumsum(e64[order])
     target = top_p * total
@@ -63,20 +63,23 @@ def kept_set(e: np.ndarray, top_p: float) -> tuple[np.ndarray, float]:
     keep = np.zeros(e.size, dtype=bool)
     keep[order[: k + 1]] = True
     before = cum[k - 1] if k > 0 else 0.0
-    margin = min(abs(cum[k] - target), abs(target - before)) / total
-    return keep, float(margin)
+    over, under = abs(cum[k] - target), abs(target - before)
+    alt = keep.copy()
+    if over <= under and k + 1 < e.size:
+        alt[order[k + 1]] = True  # the crossing prefix judged one token short
+    elif k > 0:
+        alt[order[k]] = False  # the prefix before the crossing judged long enough
+    return keep, float(min(over, under) / total), alt
 
 
-def sample_row(z, temperature: float, top_p: float, u: float) -> tuple[int, float]:
-    """Return (token id, margin) for one row of logits.
+def kept_set(e: np.ndarray, top_p: float) -> tuple[np.ndarray, float]:
+    """Boolean mask of the nucleus and the top-p margin (relative to S)."""
+    keep, margin, _ = _kept(e, top_p)
+    return keep, margin
 
-    margin is the top-2 logit gap for greedy rows, otherwise the smallest
-    relative distance of the decision from flipping (top-p crossing or CDF edge).
-    """
-    if temperature == 0.0:
-        return _greedy(z)
-    e = decision_values(z, temperature)
-    keep, m_top = kept_set(e, top_p)
+
+def _draw(e: np.ndarray, keep: np.ndarray, u: float) -> tuple[int, float]:
+    """Inverse-CDF draw over the kept ids in ascending order; (token, CDF-edge margin)."""
     ids = np.nonzero(keep)[0]  # ascending id
     w = e[ids].astype(np.float64)
     mass = w.sum()
@@ -86,8 +89,28 @@ def sample_row(z, temperature: float, top_p: float, u: float) -> tuple[int, floa
     if j >= ids.size:
         j = ids.size - 1
     lo = c[j - 1] if j > 0 else 0.0
-    m_cdf = min(abs(c[j] - thresh), abs(thresh - lo)) / mass
-    return int(ids[j]), float(min(m_top, m_cdf))
+    return int(ids[j]), float(min(abs(c[j] - thresh), abs(thresh - lo)) / mass)
+
+
+def sample_row(z, temperature: float, top_p: float, u: float) -> tuple[int, float]:
+    """Return (token id, margin) for one row of logits.
+
+    margin is the top-2 logit gap for greedy rows, otherwise the smallest
+    relative distance of the decision from flipping: the CDF edges around the
+    draw and, when flipping the top-p crossing would change the drawn token,
+    the top-p crossing itself.
+    """
+    if temperature == 0.0:
+        return _greedy(z)
+    e = decision_values(z, temperature)
+    keep, m_top, alt = _kept(e, top_p)
+    tok, m_cdf = _draw(e, keep, u)
+    if alt is None or not alt.any():
+        return tok, min(m_top, m_cdf)
+    tok_alt, m_alt = _draw(e, alt, u)
+    if tok_alt == tok:  # either reading of the crossing draws the same token
+        return tok, min(m_cdf, m_alt)
+    return tok, min(m_top, m_cdf)
 
 
 def sample_batch(logits: np.ndarray, temperature: float, top_p: float, u: np.ndarray):

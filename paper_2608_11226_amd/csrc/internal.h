@@ -1,0 +1,143 @@
+// Internal declarations shared by the kernels and the host runtime of librollout.
+// Not part of the public ABI (that is include/rollout.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rollout.h"
+
+namespace rollout {
+
+// ---------------------------------------------------------------------------
+// Model dimensions as the kernels see them.
+// ---------------------------------------------------------------------------
+struct Dims {
+  int L, d, nh, nkv, hd, ff, V;
+  int qd, kvd, nqkv;  // nh*hd, nkv*hd, qd + 2*kvd
+  float eps, theta;
+  int dtype;          // ROLLOUT_DTYPE_*
+  int blk;            // tokens per KV block
+  int max_ctx;        // max prompt + max new tokens
+};
+
+// Bytes of one cache element and one weight element.
+inline size_t elem_bytes(int dtype) { return dtype == ROLLOUT_DTYPE_BF16 ? 2 : 4; }
+
+// Physical layout of a weight matrix.
+enum WLayout : int {
+  W_ROWMAJOR = 0,  // [rows][cols]
+  W_TILED = 1,     // MFMA operand tiles [rows/16][cols/32][64 lanes][8], lane = r%16 + 16*((c%32)/8)
+};
+
+// How physical rows of a (possibly fused) matrix map to synthesis tensor ids.
+enum WFuse : int {
+  FUSE_NONE = 0,  // one tensor: id0, row = physical row
+  FUSE_QKV = 1,   // rows [0,a) id0, [a,a+b) id1, [a+b,a+2b) id2
+  FUSE_GU = 2,    // 16-row blocks alternate id0 (gate) and id1 (up)
+};
+
+struct WeightDesc {
+  int rows, cols;
+  int layout;  // WLayout
+  int fuse;    // WFuse
+  int id0, id1, id2;
+  int a, b;    // FUSE_QKV split sizes (q rows, kv rows)
+};
+
+// Where each activation row of a prefill or decode pass lives in the cache.
+//   decode  (P == 0): row m is sequence seq0 + m at position ctx_len[m].
+//   prefill (P > 0):  row m is token t = m % P of prompt m / P; it belongs to
+//                     sequence seq0 + (m / P) * G at position t, and its K/V go
+//                     to all G sequences of the group when t lies in the last,
+//                     partially filled prompt block (shared blocks otherwise).
+struct RowMap {
+  const int32_t* ctx_len;
+  int P, G, seq0;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (each enqueues on the given stream and returns hipGetLastError()).
+// ---------------------------------------------------------------------------
+hipError_t launch_synth(hipStream_t s, void* dst, int dtype, const WeightDesc& w, uint64_t seed, double std_);
+hipError_t launch_fill(hipStream_t s, float* dst, size_t n, float value);
+hipError_t launch_export(hipStream_t s, const void* src, int dtype, const WeightDesc& w, int which, int rows,
+                         float* out);
+
+// out[split][m][n] = sum over the split's k range of X[m][k] * W[n][k] (fp32).
+int gemm_splits(int dtype, int M, int N, int K, int max_splits);
+hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const void* W, float* out, int M,
+                       int N, int K, int splits);
+
+hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
+                        const int32_t* col, int M, int d, int V, float* x, int32_t* err);
+// x[m] += sum_s part[s][m] (part may be NULL); out[m] = rmsnorm(x[m]) * gain in the cache dtype.
+hipError_t launch_residual_norm(hipStream_t s, int dtype, const float* part, int splits, int M, int d, float* x,
+                                const float* gain, float eps, void* out);
+hipError_t launch_qkv_epilogue(hipStream_t s, const Dims& D, const float* part, int splits, int M, RowMap rm,
+                               const float* rope_cos, const float* rope_sin, void* q_out, void* kv_pool,
+                               int n_blocks, const int32_t* tables, int max_blocks, int layer, int32_t* err);
+hipError_t launch_swiglu(hipStream_t s, int dtype, const float* part, int splits, int M, int ff, void* h);
+int attn_splits(int max_ctx, int* split_tokens);
+hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const void* kv_pool, int n_blocks,
+                            const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
+                            int layer, float* opart, float* ml, int32_t* err);
+hipError_t launch_attn_combine(hipStream_t s, const Dims& D, const float* opart, const float* ml, int R,
+                               int splits, void* out);
+hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
+                              void* dst);
+hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);
+hipError_t launch_set_cols(hipStream_t s, int32_t* cols, int c0, int c1);
+hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float temperature, float top_p,
+                         const float* u, int u_stride, const int32_t* col, int32_t* out, int out_stride);
+hipError_t launch_grpo(hipStream_t s, const float* r, int n_groups, int G, float eps, int ddof, float* adv,
+                       int32_t* zero_var);
+
+}  // namespace rollout
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+#ifdef __HIPCC__
+namespace rollout {
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float ldf(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ float ldf(const uint16_t* p, size_t i) { return bf16_to_f32(p[i]); }
+__device__ __forceinline__ void stf(float* p, size_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void stf(uint16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Sum over the whole block in a fixed order (deterministic); red holds >= 32 floats.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+}  // namespace rollout
+#endif

@@ -1,0 +1,793 @@
+// Host runtime of librollout: the C ABI, the planner that sizes sequences in
+// flight to the HBM budget, the arena layout, the paged-KV block manager and
+// the launch sequences of prefill, decode and whole rollouts.
+//
+// A GRPO step's rollout phase (section 3 of the paper) generates G
+// completions for each of B prompts; the generation batch is kept a multiple
+// of G (section 4.3), and the concurrency it runs at is the knob that moves
+// power and throughput (section 6.4, Table 4).  Group size, sequences in
+// flight, completion length, temperature and top-p are therefore arguments of
+// every call, never state fixed at initialisation.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace rollout;
+
+namespace {
+
+thread_local std::string g_last_error = "";
+
+constexpr size_t kAlign = 256;
+constexpr int kPrefillRows = 4096;  // activation rows of one prefill chunk (whole prompts)
+constexpr int kMaxSplits = 16;      // K splits of one projection GEMM
+
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Layer {
+  size_t wqkv, wo, wgu, wdown, attn_norm, mlp_norm;
+};
+
+// Byte offsets of everything in the arena.
+struct Layout {
+  size_t embed = 0, lm_head = 0, final_norm = 0;
+  std::vector<Layer> layers;
+  size_t rope_cos = 0, rope_sin = 0;
+  size_t weights_end = 0;  // weights + rope tables
+  size_t x = 0, a = 0, q = 0, o = 0, h = 0, a_last = 0, part = 0, opart = 0, ml = 0, logits = 0;
+  size_t tables = 0, ctx_len = 0, cols = 0, err = 0;
+  size_t work_end = 0;     // start of the KV pool
+  size_t weight_bytes = 0, work_bytes = 0, kv_block_bytes = 0;
+  int S = 0, R = 0, T_chunk = 0, max_blocks = 0, attn_splits_max = 1;
+  size_t part_elems = 0;
+};
+
+Dims make_dims(const rollout_model_config& c) {
+  Dims D;
+  D.L = c.n_layers;
+  D.d = c.d_model;
+  D.nh = c.n_heads;
+  D.nkv = c.n_kv_heads;
+  D.hd = c.head_dim;
+  D.ff = c.d_ff;
+  D.V = c.vocab;
+  D.qd = c.n_heads * c.head_dim;
+  D.kvd = c.n_kv_heads * c.head_dim;
+  D.nqkv = D.qd + 2 * D.kvd;
+  D.eps = c.rms_eps;
+  D.theta = c.rope_theta;
+  D.dtype = c.dtype;
+  D.blk = c.kv_block_size;
+  D.max_ctx = c.max_prompt_len + c.max_new_tokens;
+  return D;
+}
+
+// Returns ROLLOUT_OK or an error code with *msg set.
+rollout_status validate_config(const rollout_model_config* c, std::string* msg) {
+  if (!c) { *msg = "config is NULL"; return ROLLOUT_EINVAL; }
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->n_kv_heads < 1 || c->head_dim < 1 ||
+      c->d_ff < 1 || c->vocab < 2) {
+    *msg = "model dimensions must be positive (vocab >= 2)";
+    return ROLLOUT_EINVAL;
+  }
+  if (c->dtype != ROLLOUT_DTYPE_FP32 && c->dtype != ROLLOUT_DTYPE_BF16) { *msg = "dtype must be 0 (fp32) or 1 (bf16)"; return ROLLOUT_EINVAL; }
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f) || !(c->weight_std > 0.0)) {
+    *msg = "rms_eps > 0, rope_theta > 1 and weight_std > 0 are required";
+    return ROLLOUT_EINVAL;
+  }
+  if (c->max_prompt_len < 1 || c->max_new_tokens < 1 || c->max_seqs_in_flight < 1) {
+    *msg = "max_prompt_len, max_new_tokens and max_seqs_in_flight must be >= 1";
+    return ROLLOUT_EINVAL;
+  }
+  if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) { *msg = "head_dim must be 32, 64 or 128"; return ROLLOUT_EUNSUPPORTED; }
+  if (c->n_heads % c->n_kv_heads || c->n_heads / c->n_kv_heads > 16) {
+    *msg = "n_heads must be a multiple of n_kv_heads, at most 16 query heads per KV head";
+    return ROLLOUT_EUNSUPPORTED;
+  }
+  if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32 || c->d_ff % 32 || c->vocab % 16) {
+    *msg = "d_model, n_heads*head_dim and d_ff must be multiples of 32, vocab a multiple of 16";
+    return ROLLOUT_EUNSUPPORTED;
+  }
+  if (c->kv_block_size != 8 && c->kv_block_size != 16 && c->kv_block_size != 32) {
+    *msg = "kv_block_size must be 8, 16 or 32";
+    return ROLLOUT_EUNSUPPORTED;
+  }
+  if ((int64_t)c->max_prompt_len + c->max_new_tokens > (1 << 20)) { *msg = "context longer than 2^20 tokens"; return ROLLOUT_EUNSUPPORTED; }
+  if ((int64_t)c->vocab * c->d_model > ((int64_t)1 << 31) - 1 || (int64_t)c->d_ff * 2 * c->d_model > ((int64_t)1 << 31) - 1) {
+    *msg = "a weight matrix exceeds 2^31 elements";
+    return ROLLOUT_EUNSUPPORTED;
+  }
+  return ROLLOUT_OK;
+}
+
+int prefill_chunk_rows(int max_prompt_len) {
+  return std::max(max_prompt_len, kPrefillRows / max_prompt_len * max_prompt_len);
+}
+
+size_t max_part_elems(const Dims& D, int R) {
+  size_t best = 0;
+  const int Ns[4] = {D.nqkv, D.d, 2 * D.ff, D.d};
+  const int Ks[4] = {D.d, D.qd, D.d, D.ff};
+  for (int M = 1; M <= R; ++M)
+    for (int j = 0; j < 4; ++j) {
+      const int s = gemm_splits(D.dtype, M, Ns[j], Ks[j], kMaxSplits);
+      best = std::max(best, (size_t)s * (size_t)M * (size_t)Ns[j]);
+    }
+  return best;
+}
+
+// Layout of weights and work buffers for S sequences in flight; the KV pool follows work_end.
+Layout make_layout(const Dims& D, int S, int max_prompt_len) {
+  Layout Lo;
+  const size_t eb = elem_bytes(D.dtype);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  Lo.embed = take((size_t)D.V * D.d * eb);
+  Lo.layers.resize(D.L);
+  for (int l = 0; l < D.L; ++l) {
+    Layer& y = Lo.layers[l];
+    y.wqkv = take((size_t)D.nqkv * D.d * eb);
+    y.wo = take((size_t)D.d * D.qd * eb);
+    y.wgu = take((size_t)2 * D.ff * D.d * eb);
+    y.wdown = take((size_t)D.d * D.ff * eb);
+    y.attn_norm = take((size_t)D.d * 4);
+    y.mlp_norm = take((size_t)D.d * 4);
+  }
+  Lo.final_norm = take((size_t)D.d * 4);
+  Lo.lm_head = take((size_t)D.V * D.d * eb);
+  Lo.weight_bytes = off;
+  Lo.rope_cos = take((size_t)D.max_ctx * (D.hd / 2) * 4);
+  Lo.rope_sin = take((size_t)D.max_ctx * (D.hd / 2) * 4);
+  Lo.weights_end = off;
+
+  Lo.S = S;
+  Lo.T_chunk = prefill_chunk_rows(max_prompt_len);
+  Lo.R = std::max(S, Lo.T_chunk);
+  Lo.max_blocks = (D.max_ctx + D.blk - 1) / D.blk;
+  int st;
+  Lo.attn_splits_max = attn_splits(D.max_ctx, &st);
+  Lo.part_elems = max_part_elems(D, Lo.R);
+  const size_t R = Lo.R;
+  Lo.x = take(R * D.d * 4);
+  Lo.a = take(R * std::max(D.d, D.qd) * eb);
+  Lo.q = take(R * D.qd * eb);
+  Lo.o = take(R * D.qd * eb);
+  Lo.h = take(R * D.ff * eb);
+  Lo.a_last = take((size_t)S * D.d * eb);
+  Lo.part = take(Lo.part_elems * 4);
+  Lo.opart = take(R * D.nh * Lo.attn_splits_max * D.hd * 4);
+  Lo.ml = take(R * D.nh * Lo.attn_splits_max * 2 * 4);
+  Lo.logits = take((size_t)S * D.V * 4);
+  Lo.tables = take((size_t)S * Lo.max_blocks * 4 + (size_t)S * 4);  // block tables, then ctx_len
+  Lo.ctx_len = Lo.tables + (size_t)S * Lo.max_blocks * 4;
+  Lo.cols = take(64);
+  Lo.err = take(64);
+  Lo.work_end = off;
+  Lo.work_bytes = Lo.work_end - Lo.weights_end;
+  Lo.kv_block_bytes = (size_t)D.L * D.nkv * 2 * D.blk * D.hd * eb;
+  return Lo;
+}
+
+// KV blocks for n_prompts groups of G sequences of up to ctx tokens whose first P tokens are shared.
+int64_t blocks_needed(int n_prompts, int G, int P, int ctx, int blk) {
+  const int64_t shared = P / blk;
+  const int64_t per_seq = (ctx + blk - 1) / blk - shared;
+  return (int64_t)n_prompts * shared + (int64_t)n_prompts * G * per_seq;
+}
+
+struct Prof {
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  struct Rec { int cls; int e0, e1; double bytes, flops; };
+  std::vector<Rec> recs;
+};
+
+}  // namespace
+
+struct rollout_ctx {
+  rollout_model_config cfg;
+  Dims D;
+  Layout Lo;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  char* arena = nullptr;
+  uint64_t arena_bytes = 0;
+  int n_blocks = 0;
+  std::string err;
+
+  // host staging (pinned) for block tables and context lengths
+  int32_t* h_tables = nullptr;
+
+  // current wave
+  bool wave = false;
+  int S = 0, P = 0, G = 0, cur_len = 0, n_prompts = 0;
+
+  Prof prof;
+
+  template <typename T = void>
+  T* at(size_t off) const { return reinterpret_cast<T*>(arena + off); }
+};
+
+namespace {
+
+rollout_status fail(rollout_ctx* c, rollout_status st, const std::string& msg) {
+  if (c) c->err = msg;
+  g_last_error = msg;
+  return st;
+}
+
+rollout_status hip_fail(rollout_ctx* c, hipError_t e, const char* where) {
+  return fail(c, ROLLOUT_EDEVICE, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(ctx, expr, where)                  \
+  do {                                             \
+    hipError_t e_ = (expr);                        \
+    if (e_ != hipSuccess) return hip_fail(ctx, e_, where); \
+  } while (0)
+
+WeightDesc wdesc(int rows, int cols, int layout, int fuse, int id0, int id1 = 0, int id2 = 0, int a = 0, int b = 0) {
+  WeightDesc w;
+  w.rows = rows;
+  w.cols = cols;
+  w.layout = layout;
+  w.fuse = fuse;
+  w.id0 = id0;
+  w.id1 = id1;
+  w.id2 = id2;
+  w.a = a;
+  w.b = b;
+  return w;
+}
+
+int matrix_layout(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 ? W_TILED : W_ROWMAJOR; }
+
+// ---------------------------------------------------------------------------
+// profiling hooks (HIP events around launches on the context stream)
+// ---------------------------------------------------------------------------
+struct Scope {
+  rollout_ctx* c;
+  int cls;
+  double bytes, flops;
+  int e0 = -1;
+  Scope(rollout_ctx* c_, int cls_, double bytes_, double flops_) : c(c_), cls(cls_), bytes(bytes_), flops(flops_) {
+    if (!c->prof.on) return;
+    e0 = (int)c->prof.recs.size() * 2;
+    while ((int)c->prof.ev.size() < e0 + 2) {
+      hipEvent_t e;
+      hipEventCreate(&e);
+      c->prof.ev.push_back(e);
+    }
+    hipEventRecord(c->prof.ev[e0], c->stream);
+  }
+  ~Scope() {
+    if (!c->prof.on) return;
+    hipEventRecord(c->prof.ev[e0 + 1], c->stream);
+    c->prof.recs.push_back({cls, e0, e0 + 1, bytes, flops});
+  }
+};
+
+rollout_status gemm(rollout_ctx* c, const void* X, const void* W, float* out, int M, int N, int K, int max_splits,
+                    int* splits_out) {
+  const Dims& D = c->D;
+  const int s = gemm_splits(D.dtype, M, N, K, max_splits);
+  if ((size_t)s * M * N > c->Lo.part_elems && out == c->at<float>(c->Lo.part))
+    return fail(c, ROLLOUT_EINVAL, "internal: split-K workspace too small");
+  const double eb = (double)elem_bytes(D.dtype);
+  Scope sc(c, 0, (double)N * K * eb + (double)M * K * eb + (double)M * N * 4, 2.0 * M * N * K);
+  HIP_TRY(c, launch_gemm(c->stream, D.dtype, X, K, W, out, M, N, K, s), "gemm");
+  *splits_out = s;
+  return ROLLOUT_OK;
+}
+
+// One transformer pass over M rows (prefill chunk or decode batch). On return
+// c->Lo.a holds the final-normed hidden states (cache dtype).
+rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max, double kv_tokens_read) {
+  const Dims& D = c->D;
+  const Layout& Lo = c->Lo;
+  float* x = c->at<float>(Lo.x);
+  void* a = c->at(Lo.a);
+  void* q = c->at(Lo.q);
+  void* o = c->at(Lo.o);
+  void* h = c->at(Lo.h);
+  float* part = c->at<float>(Lo.part);
+  float* opart = c->at<float>(Lo.opart);
+  float* ml = c->at<float>(Lo.ml);
+  int32_t* err = c->at<int32_t>(Lo.err);
+  const int32_t* tables = c->at<int32_t>(Lo.tables);
+  char* kv = c->arena + Lo.work_end;
+  const double eb = (double)elem_bytes(D.dtype);
+  int st_tok;
+  const int asplits = attn_splits(attn_ctx_max, &st_tok);
+  {
+    Scope sc(c, 2, (double)M * D.d * (4 + eb), 0);
+    HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, nullptr, 1, M, D.d, x, c->at<float>(Lo.layers[0].attn_norm),
+                                    D.eps, a), "rmsnorm");
+  }
+  for (int l = 0; l < D.L; ++l) {
+    const Layer& y = Lo.layers[l];
+    int s;
+    rollout_status r = gemm(c, a, c->at(y.wqkv), part, M, D.nqkv, D.d, kMaxSplits, &s);
+    if (r) return r;
+    {
+      Scope sc(c, 2, (double)s * M * D.nqkv * 4 + (double)M * (D.qd + 2 * D.kvd) * eb, 0);
+      HIP_TRY(c, launch_qkv_epilogue(c->stream, D, part, s, M, rm, c->at<float>(Lo.rope_cos), c->at<float>(Lo.rope_sin),
+                                     q, kv, c->n_blocks, tables, Lo.max_blocks, l, err), "qkv epilogue");
+    }
+    {
+      const double kvb = kv_tokens_read * D.nkv * 2.0 * D.hd * eb;
+      Scope sc(c, 1, kvb + (double)M * D.qd * (eb + eb), 4.0 * kv_tokens_read * D.nh * D.hd);
+      HIP_TRY(c, launch_attention(c->stream, D, q, kv, c->n_blocks, tables, Lo.max_blocks, rm, M, asplits, st_tok, l,
+                                  opart, ml, err), "attention");
+      HIP_TRY(c, launch_attn_combine(c->stream, D, opart, ml, M, asplits, o), "attention combine");
+    }
+    r = gemm(c, o, c->at(y.wo), part, M, D.d, D.qd, kMaxSplits, &s);
+    if (r) return r;
+    {
+      Scope sc(c, 2, (double)s * M * D.d * 4 + (double)M * D.d * (8 + eb), 0);
+      HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, part, s, M, D.d, x, c->at<float>(y.mlp_norm), D.eps, a),
+              "residual norm");
+    }
+    r = gemm(c, a, c->at(y.wgu), part, M, 2 * D.ff, D.d, kMaxSplits, &s);
+    if (r) return r;
+    {
+      Scope sc(c, 2, (double)s * M * 2 * D.ff * 4 + (double)M * D.ff * eb, 0);
+      HIP_TRY(c, launch_swiglu(c->stream, D.dtype, part, s, M, D.ff, h), "swiglu");
+    }
+    r = gemm(c, h, c->at(y.wdown), part, M, D.d, D.ff, kMaxSplits, &s);
+    if (r) return r;
+    {
+      const float* next_gain = l + 1 < D.L ? c->at<float>(Lo.layers[l + 1].attn_norm) : c->at<float>(Lo.final_norm);
+      Scope sc(c, 2, (double)s * M * D.d * 4 + (double)M * D.d * (8 + eb), 0);
+      HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, part, s, M, D.d, x, next_gain, D.eps, a), "residual norm");
+    }
+  }
+  return ROLLOUT_OK;
+}
+
+rollout_status upload_wave(rollout_ctx* c, int n_prompts, int P, int G) {
+  const Dims& D = c->D;
+  const Layout& Lo = c->Lo;
+  const int S = n_prompts * G;
+  const int ctx = P + c->cfg.max_new_tokens;
+  const int64_t need = blocks_needed(n_prompts, G, P, ctx, D.blk);
+  if (need > c->n_blocks)
+    return fail(c, ROLLOUT_ENOMEM, "wave needs " + std::to_string(need) + " KV blocks, pool has " +
+                                       std::to_string(c->n_blocks));
+  // the staging buffer may still feed a copy of the previous wave
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "stream sync");
+  int32_t* t = c->h_tables;
+  std::fill(t, t + (size_t)Lo.S * Lo.max_blocks, -1);
+  const int shared = P / D.blk;
+  const int nb_seq = (ctx + D.blk - 1) / D.blk;
+  int next = 0;
+  for (int p = 0; p < n_prompts; ++p) {
+    for (int j = 0; j < shared; ++j) {
+      for (int g = 0; g < G; ++g) t[(size_t)(p * G + g) * Lo.max_blocks + j] = next;
+      ++next;
+    }
+    for (int g = 0; g < G; ++g)
+      for (int j = shared; j < nb_seq; ++j) t[(size_t)(p * G + g) * Lo.max_blocks + j] = next++;
+  }
+  int32_t* ctxl = t + (size_t)Lo.S * Lo.max_blocks;
+  for (int s = 0; s < Lo.S; ++s) ctxl[s] = s < S ? P : 0;
+  HIP_TRY(c, hipMemcpyAsync(c->at(Lo.tables), t, (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipMemcpyHostToDevice,
+                            c->stream), "block table upload");
+  c->wave = true;
+  c->S = S;
+  c->P = P;
+  c->G = G;
+  c->n_prompts = n_prompts;
+  c->cur_len = P;
+  return ROLLOUT_OK;
+}
+
+rollout_status do_prefill(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G, float* d_logits) {
+  const Dims& D = c->D;
+  const Layout& Lo = c->Lo;
+  rollout_status r = upload_wave(c, n_prompts, P, G);
+  if (r) return r;
+  const int per_chunk = std::max(1, Lo.T_chunk / P);
+  for (int p0 = 0; p0 < n_prompts; p0 += per_chunk) {
+    const int np = std::min(per_chunk, n_prompts - p0);
+    const int M = np * P;
+    {
+      Scope sc(c, 2, (double)M * D.d * (4 + elem_bytes(D.dtype)), 0);
+      HIP_TRY(c, launch_embed(c->stream, D.dtype, c->at(Lo.embed), d_prompts + (size_t)p0 * P, 1, nullptr, M, D.d, D.V,
+                              c->at<float>(Lo.x), c->at<int32_t>(Lo.err)), "embed");
+    }
+    RowMap rm{nullptr, P, G, p0 * G};
+    r = forward_layers(c, M, rm, P, (double)np * P * (P + 1) / 2.0);
+    if (r) return r;
+    HIP_TRY(c, launch_gather_rows(c->stream, D.dtype, c->at(Lo.a), D.d, P, G, np, c->at(Lo.a_last)), "gather");
+    int s;
+    r = gemm(c, c->at(Lo.a_last), c->at(Lo.lm_head), d_logits + (size_t)p0 * G * D.V, np * G, D.V, D.d, 1, &s);
+    if (r) return r;
+  }
+  return ROLLOUT_OK;
+}
+
+// Enqueue one decode step of the current wave (no host-side state change).
+rollout_status enqueue_decode(rollout_ctx* c, const int32_t* tokens, int tok_stride, const int32_t* col,
+                              float* d_logits, int ctx_max) {
+  const Dims& D = c->D;
+  const Layout& Lo = c->Lo;
+  const int S = c->S;
+  {
+    Scope sc(c, 2, (double)S * D.d * (4 + elem_bytes(D.dtype)), 0);
+    HIP_TRY(c, launch_embed(c->stream, D.dtype, c->at(Lo.embed), tokens, tok_stride, col, S, D.d, D.V,
+                            c->at<float>(Lo.x), c->at<int32_t>(Lo.err)), "embed");
+  }
+  RowMap rm{c->at<int32_t>(Lo.ctx_len), 0, 1, 0};
+  rollout_status r = forward_layers(c, S, rm, ctx_max, (double)S * (c->cur_len + 1));
+  if (r) return r;
+  int s;
+  r = gemm(c, c->at(Lo.a), c->at(Lo.lm_head), d_logits, S, D.V, D.d, 1, &s);
+  if (r) return r;
+  HIP_TRY(c, launch_advance(c->stream, c->at<int32_t>(Lo.ctx_len), S, nullptr), "advance");
+  return ROLLOUT_OK;
+}
+
+void rope_tables(const Dims& D, std::vector<float>* cs, std::vector<float>* sn) {
+  const int half = D.hd / 2;
+  cs->resize((size_t)D.max_ctx * half);
+  sn->resize((size_t)D.max_ctx * half);
+  for (int i = 0; i < half; ++i) {
+    const double inv = std::pow((double)D.theta, -(2.0 * i) / (double)D.hd);
+    for (int p = 0; p < D.max_ctx; ++p) {
+      const double ang = (double)p * inv;
+      (*cs)[(size_t)p * half + i] = (float)std::cos(ang);
+      (*sn)[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  }
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* rollout_last_error(const rollout_ctx* ctx) {
+  if (ctx) return ctx->err.c_str();
+  return g_last_error.c_str();
+}
+
+rollout_status rollout_plan(const rollout_model_config* cfg, int32_t group_size, rollout_plan_t* out) {
+  std::string msg;
+  rollout_status st = validate_config(cfg, &msg);
+  if (st) return fail(nullptr, st, msg);
+  if (group_size < 1) return fail(nullptr, ROLLOUT_EINVAL, "group_size must be >= 1");
+  if (!out) return fail(nullptr, ROLLOUT_EINVAL, "out is NULL");
+  const Dims D = make_dims(*cfg);
+  uint64_t budget = cfg->hbm_budget_bytes;
+  uint64_t reserve = 0;
+  if (budget == 0) {
+    size_t free_b = 0, total_b = 0;
+    hipError_t e = hipMemGetInfo(&free_b, &total_b);
+    if (e != hipSuccess) return fail(nullptr, ROLLOUT_EDEVICE, std::string("hipMemGetInfo: ") + hipGetErrorString(e));
+    budget = free_b;
+    reserve = (uint64_t)2 << 30;  // headroom for the caller's own allocations
+  }
+  const int ctx = cfg->max_prompt_len + cfg->max_new_tokens;
+  // bytes of the arena for k whole groups in flight (weights + work for k*G rows + KV blocks)
+  auto arena_for = [&](int64_t k, Layout* lo, int64_t* nb) {
+    *lo = make_layout(D, (int)(k * group_size), cfg->max_prompt_len);
+    *nb = blocks_needed((int)k, group_size, cfg->max_prompt_len, ctx, D.blk);
+    return (uint64_t)lo->work_end + (uint64_t)*nb * lo->kv_block_bytes;
+  };
+  // the arena grows with the number of groups, so the largest fitting count is found by bisection
+  int64_t lo_k = 0, hi_k = cfg->max_seqs_in_flight / group_size;
+  Layout Lo;
+  int64_t nb = 0;
+  while (lo_k < hi_k) {
+    const int64_t mid = (lo_k + hi_k + 1) / 2;
+    if (arena_for(mid, &Lo, &nb) + reserve <= budget) lo_k = mid;
+    else hi_k = mid - 1;
+  }
+  if (lo_k < 1)
+    return fail(nullptr, ROLLOUT_ENOMEM, "not even one group of " + std::to_string(group_size) +
+                                             " sequences fits in the HBM budget");
+  const uint64_t total = arena_for(lo_k, &Lo, &nb);
+  out->seqs_in_flight_max = (int32_t)(lo_k * group_size);
+  out->kv_blocks = (int32_t)nb;
+  out->arena_bytes = total;
+  out->weight_bytes = Lo.weight_bytes;
+  out->kv_block_bytes = Lo.kv_block_bytes;
+  out->kv_bytes = (uint64_t)nb * Lo.kv_block_bytes;
+  out->work_bytes = Lo.work_end - Lo.weight_bytes;
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_init(const rollout_model_config* cfg, void* d_arena, uint64_t arena_bytes, void* hip_stream,
+                            rollout_ctx** out) {
+  std::string msg;
+  rollout_status st = validate_config(cfg, &msg);
+  if (st) return fail(nullptr, st, msg);
+  if (!out || !d_arena) return fail(nullptr, ROLLOUT_EINVAL, "arena and out must be non-NULL");
+  if ((uintptr_t)d_arena % kAlign) return fail(nullptr, ROLLOUT_EINVAL, "arena must be 256-byte aligned");
+  const Dims D = make_dims(*cfg);
+  Layout Lo = make_layout(D, cfg->max_seqs_in_flight, cfg->max_prompt_len);
+  if (arena_bytes < Lo.work_end + Lo.kv_block_bytes * (uint64_t)Lo.max_blocks)
+    return fail(nullptr, ROLLOUT_ENOMEM, "arena of " + std::to_string(arena_bytes) + " bytes holds no sequence (needs " +
+                                             std::to_string(Lo.work_end + Lo.kv_block_bytes * Lo.max_blocks) + ")");
+  const uint64_t nb = (arena_bytes - Lo.work_end) / Lo.kv_block_bytes;
+  rollout_ctx* c = new rollout_ctx();
+  c->cfg = *cfg;
+  c->D = D;
+  c->Lo = Lo;
+  c->arena = (char*)d_arena;
+  c->arena_bytes = arena_bytes;
+  c->n_blocks = (int)std::min<uint64_t>(nb, (uint64_t)INT32_MAX);
+  if (hip_stream) {
+    c->stream = (hipStream_t)hip_stream;
+  } else {
+    hipError_t e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+    if (e != hipSuccess) { delete c; return fail(nullptr, ROLLOUT_EDEVICE, std::string("stream: ") + hipGetErrorString(e)); }
+    c->own_stream = true;
+  }
+  hipError_t e = hipHostMalloc((void**)&c->h_tables, (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    rollout_destroy(c);
+    return fail(nullptr, ROLLOUT_EDEVICE, std::string("pinned staging: ") + hipGetErrorString(e));
+  }
+  auto bad = [&](hipError_t err, const char* where) {
+    std::string m = std::string(where) + ": " + hipGetErrorString(err);
+    rollout_destroy(c);
+    return fail(nullptr, ROLLOUT_EDEVICE, m);
+  };
+  // weights, straight into the layouts the kernels read
+  const int lay = matrix_layout(D);
+  const uint64_t seed = cfg->weight_seed;
+  const double sd = cfg->weight_std;
+  if ((e = launch_synth(c->stream, c->at(Lo.embed), D.dtype, wdesc(D.V, D.d, W_ROWMAJOR, FUSE_NONE, 0), seed, sd)))
+    return bad(e, "synth embed");
+  for (int l = 0; l < D.L; ++l) {
+    const Layer& y = Lo.layers[l];
+    const int b = 1 + 9 * l;
+    if ((e = launch_synth(c->stream, c->at(y.wqkv), D.dtype, wdesc(D.nqkv, D.d, lay, FUSE_QKV, b + 1, b + 2, b + 3, D.qd, D.kvd), seed, sd)) ||
+        (e = launch_synth(c->stream, c->at(y.wo), D.dtype, wdesc(D.d, D.qd, lay, FUSE_NONE, b + 4), seed, sd)) ||
+        (e = launch_synth(c->stream, c->at(y.wgu), D.dtype, wdesc(2 * D.ff, D.d, lay, FUSE_GU, b + 6, b + 7), seed, sd)) ||
+        (e = launch_synth(c->stream, c->at(y.wdown), D.dtype, wdesc(D.d, D.ff, lay, FUSE_NONE, b + 8), seed, sd)) ||
+        (e = launch_fill(c->stream, c->at<float>(y.attn_norm), D.d, 1.0f)) ||
+        (e = launch_fill(c->stream, c->at<float>(y.mlp_norm), D.d, 1.0f)))
+      return bad(e, "synth layer");
+  }
+  if ((e = launch_fill(c->stream, c->at<float>(Lo.final_norm), D.d, 1.0f)) ||
+      (e = launch_synth(c->stream, c->at(Lo.lm_head), D.dtype, wdesc(D.V, D.d, lay, FUSE_NONE, 2 + 9 * D.L), seed, sd)))
+    return bad(e, "synth head");
+  std::vector<float> cs, sn;
+  rope_tables(D, &cs, &sn);
+  if ((e = hipMemcpyAsync(c->at(Lo.rope_cos), cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c->stream)) ||
+      (e = hipMemcpyAsync(c->at(Lo.rope_sin), sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c->stream)) ||
+      (e = hipMemsetAsync(c->at(Lo.err), 0, 64, c->stream)) ||
+      (e = hipMemsetAsync(c->at(Lo.cols), 0, 64, c->stream)) ||
+      (e = hipStreamSynchronize(c->stream)))
+    return bad(e, "init upload");
+  *out = c;
+  return ROLLOUT_OK;
+}
+
+void rollout_destroy(rollout_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->stream) hipStreamSynchronize(ctx->stream);
+  for (hipEvent_t e : ctx->prof.ev) hipEventDestroy(e);
+  if (ctx->h_tables) hipHostFree(ctx->h_tables);
+  if (ctx->own_stream) hipStreamDestroy(ctx->stream);
+  delete ctx;
+}
+
+rollout_status rollout_prefill(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts, int32_t prompt_len,
+                               int32_t group_size, float* d_logits) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!d_prompts || !d_logits) return fail(ctx, ROLLOUT_EINVAL, "prompts and logits must be non-NULL");
+  if (n_prompts < 1 || group_size < 1) return fail(ctx, ROLLOUT_EINVAL, "n_prompts and group_size must be >= 1");
+  if (prompt_len < 1 || prompt_len > ctx->cfg.max_prompt_len)
+    return fail(ctx, ROLLOUT_EINVAL, "prompt_len must be in [1, max_prompt_len]");
+  if ((int64_t)n_prompts * group_size > ctx->Lo.S)
+    return fail(ctx, ROLLOUT_ENOMEM, "n_prompts * group_size exceeds the sequences in flight of the context");
+  ctx->wave = false;
+  return do_prefill(ctx, d_prompts, n_prompts, prompt_len, group_size, d_logits);
+}
+
+rollout_status rollout_decode_step(rollout_ctx* ctx, const int32_t* d_tokens, float* d_logits) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!d_tokens || !d_logits) return fail(ctx, ROLLOUT_EINVAL, "tokens and logits must be non-NULL");
+  if (!ctx->wave) return fail(ctx, ROLLOUT_ESTATE, "decode before prefill");
+  if (ctx->cur_len + 1 > ctx->P + ctx->cfg.max_new_tokens)
+    return fail(ctx, ROLLOUT_ESTATE, "context full (max_prompt_len + max_new_tokens reached)");
+  rollout_status r = enqueue_decode(ctx, d_tokens, 1, nullptr, d_logits, ctx->P + ctx->cfg.max_new_tokens);
+  if (r) return r;
+  ctx->cur_len += 1;
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_sample(rollout_ctx* ctx, const float* d_logits, int32_t n_seqs, float temperature, float top_p,
+                              const float* d_uniforms, int32_t* d_tokens_out) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!d_logits || !d_uniforms || !d_tokens_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
+  if (n_seqs < 1) return fail(ctx, ROLLOUT_EINVAL, "n_seqs must be >= 1");
+  if (!(temperature >= 0.f) || !std::isfinite(temperature)) return fail(ctx, ROLLOUT_EINVAL, "temperature must be >= 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(ctx, ROLLOUT_EINVAL, "top_p must be in (0, 1]");
+  Scope sc(ctx, 2, (double)n_seqs * ctx->D.V * 4, 0);
+  HIP_TRY(ctx, launch_sample(ctx->stream, d_logits, n_seqs, ctx->D.V, temperature, top_p, d_uniforms, 1, nullptr,
+                             d_tokens_out, 1), "sample");
+  return ROLLOUT_OK;
+}
+
+rollout_status grpo_advantages(const float* d_rewards, int32_t n_groups, int32_t group_size, float eps,
+                               int32_t std_ddof, float* d_adv, int32_t* d_zero_var_groups, void* hip_stream) {
+  if (!d_rewards || !d_adv) return fail(nullptr, ROLLOUT_EINVAL, "rewards and advantages must be non-NULL");
+  if (n_groups < 1 || group_size < 1) return fail(nullptr, ROLLOUT_EINVAL, "n_groups and group_size must be >= 1");
+  if (std_ddof != 0 && std_ddof != 1) return fail(nullptr, ROLLOUT_EINVAL, "std_ddof must be 0 or 1");
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(nullptr, ROLLOUT_EINVAL, "eps must be >= 0");
+  hipError_t e = launch_grpo((hipStream_t)hip_stream, d_rewards, n_groups, group_size, eps, std_ddof, d_adv,
+                             d_zero_var_groups);
+  if (e != hipSuccess) return fail(nullptr, ROLLOUT_EDEVICE, std::string("grpo: ") + hipGetErrorString(e));
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts, int32_t prompt_len,
+                                int32_t group_size, int32_t seqs_in_flight, int32_t max_new_tokens, float temperature,
+                                float top_p, const float* d_uniforms, int32_t* d_tokens_out) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!d_prompts || !d_uniforms || !d_tokens_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
+  if (n_prompts < 1 || group_size < 1 || seqs_in_flight < 1)
+    return fail(ctx, ROLLOUT_EINVAL, "n_prompts, group_size and seqs_in_flight must be >= 1");
+  if (prompt_len < 1 || prompt_len > ctx->cfg.max_prompt_len)
+    return fail(ctx, ROLLOUT_EINVAL, "prompt_len must be in [1, max_prompt_len]");
+  if (max_new_tokens < 1 || max_new_tokens > ctx->cfg.max_new_tokens)
+    return fail(ctx, ROLLOUT_EINVAL, "max_new_tokens must be in [1, config max_new_tokens]");
+  if (!(temperature >= 0.f) || !std::isfinite(temperature)) return fail(ctx, ROLLOUT_EINVAL, "temperature must be >= 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(ctx, ROLLOUT_EINVAL, "top_p must be in (0, 1]");
+  const Dims& D = ctx->D;
+  // sequences per wave: whole groups, within the context's rows and the KV pool
+  int S = std::min<int64_t>(seqs_in_flight, ctx->Lo.S) / group_size * group_size;
+  const int ctxlen = prompt_len + ctx->cfg.max_new_tokens;
+  while (S >= group_size && blocks_needed(S / group_size, group_size, prompt_len, ctxlen, D.blk) > ctx->n_blocks)
+    S -= group_size;
+  if (S < group_size) return fail(ctx, ROLLOUT_ENOMEM, "one group does not fit in the context");
+  const int per_wave = S / group_size;
+  float* logits = ctx->at<float>(ctx->Lo.logits);
+  int32_t* cols = ctx->at<int32_t>(ctx->Lo.cols);
+  const int N = max_new_tokens;
+  for (int p0 = 0; p0 < n_prompts; p0 += per_wave) {
+    const int np = std::min(per_wave, n_prompts - p0);
+    const int s0 = p0 * group_size;
+    const int Sw = np * group_size;
+    ctx->wave = false;
+    rollout_status r = do_prefill(ctx, d_prompts + (size_t)p0 * prompt_len, np, prompt_len, group_size, logits);
+    if (r) return r;
+    int32_t* tok = d_tokens_out + (size_t)s0 * N;
+    const float* uu = d_uniforms + (size_t)s0 * N;
+    HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, nullptr, tok, N), "sample");
+    if (N == 1) continue;
+    HIP_TRY(ctx, launch_set_cols(ctx->stream, cols, 0, 1), "set cols");
+    const bool use_graph = !ctx->prof.on;
+    // cols[0] = column of the token fed in, cols[1] = column drawn; both move on after the draw
+    auto step = [&]() -> rollout_status {
+      rollout_status rr = enqueue_decode(ctx, tok, N, cols, logits, prompt_len + N);
+      if (rr) return rr;
+      HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, cols + 1, tok, N), "sample");
+      HIP_TRY(ctx, launch_advance(ctx->stream, nullptr, 0, cols), "advance");
+      return ROLLOUT_OK;
+    };
+    if (!use_graph) {
+      for (int t = 1; t < N; ++t) {
+        r = step();
+        if (r) return r;
+        ctx->cur_len += 1;
+      }
+      continue;
+    }
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    HIP_TRY(ctx, hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal), "begin capture");
+    r = step();
+    hipError_t ce = hipStreamEndCapture(ctx->stream, &graph);
+    if (r) {
+      if (graph) hipGraphDestroy(graph);
+      return r;
+    }
+    if (ce != hipSuccess) return hip_fail(ctx, ce, "end capture");
+    hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    hipGraphDestroy(graph);
+    if (ie != hipSuccess) return hip_fail(ctx, ie, "graph instantiate");
+    for (int t = 1; t < N; ++t) {
+      hipError_t le = hipGraphLaunch(exec, ctx->stream);
+      if (le != hipSuccess) {
+        hipStreamSynchronize(ctx->stream);
+        hipGraphExecDestroy(exec);
+        return hip_fail(ctx, le, "graph launch");
+      }
+      ctx->cur_len += 1;
+    }
+    hipError_t se = hipStreamSynchronize(ctx->stream);
+    hipGraphExecDestroy(exec);
+    if (se != hipSuccess) return hip_fail(ctx, se, "stream sync");
+  }
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_sync(rollout_ctx* ctx) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  int32_t flag = 0;
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream), "stream sync");
+  HIP_TRY(ctx, hipMemcpy(&flag, ctx->at(ctx->Lo.err), 4, hipMemcpyDeviceToHost), "error flag read");
+  if (flag) {
+    HIP_TRY(ctx, hipMemset(ctx->at(ctx->Lo.err), 0, 4), "error flag clear");
+    std::string m = "device error flag";
+    if (flag & 1) m += ": token id outside [0, vocab)";
+    if (flag & 2) m += ": KV write outside the block pool";
+    if (flag & 4) m += ": KV read outside the block pool";
+    return fail(ctx, ROLLOUT_EINVAL, m);
+  }
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_export_weight(rollout_ctx* ctx, int32_t tensor_id, float* d_out) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!d_out) return fail(ctx, ROLLOUT_EINVAL, "out is NULL");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  const int lay = matrix_layout(D);
+  hipError_t e;
+  if (tensor_id == 0) {
+    e = launch_export(ctx->stream, ctx->at(Lo.embed), D.dtype, wdesc(D.V, D.d, W_ROWMAJOR, FUSE_NONE, 0), 0, D.V, d_out);
+  } else if (tensor_id == 2 + 9 * D.L) {
+    e = launch_export(ctx->stream, ctx->at(Lo.lm_head), D.dtype, wdesc(D.V, D.d, lay, FUSE_NONE, 0), 0, D.V, d_out);
+  } else if (tensor_id >= 1 && tensor_id < 1 + 9 * D.L) {
+    const int l = (tensor_id - 1) / 9, slot = (tensor_id - 1) % 9;
+    const Layer& y = Lo.layers[l];
+    switch (slot) {
+      case 1: case 2: case 3:
+        e = launch_export(ctx->stream, ctx->at(y.wqkv), D.dtype, wdesc(D.nqkv, D.d, lay, FUSE_QKV, 0, 0, 0, D.qd, D.kvd),
+                          slot - 1, slot == 1 ? D.qd : D.kvd, d_out);
+        break;
+      case 4: e = launch_export(ctx->stream, ctx->at(y.wo), D.dtype, wdesc(D.d, D.qd, lay, FUSE_NONE, 0), 0, D.d, d_out); break;
+      case 6: case 7:
+        e = launch_export(ctx->stream, ctx->at(y.wgu), D.dtype, wdesc(2 * D.ff, D.d, lay, FUSE_GU, 0), slot - 6, D.ff, d_out);
+        break;
+      case 8: e = launch_export(ctx->stream, ctx->at(y.wdown), D.dtype, wdesc(D.d, D.ff, lay, FUSE_NONE, 0), 0, D.d, d_out); break;
+      default: return fail(ctx, ROLLOUT_EINVAL, "tensor id names a norm gain, not a matrix");
+    }
+  } else {
+    return fail(ctx, ROLLOUT_EINVAL, "tensor id out of range");
+  }
+  if (e != hipSuccess) return hip_fail(ctx, e, "export");
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_profile_decode_step(rollout_ctx* ctx, const int32_t* d_tokens, float* d_logits,
+                                           rollout_step_profile* out) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!out) return fail(ctx, ROLLOUT_EINVAL, "out is NULL");
+  ctx->prof.recs.clear();
+  ctx->prof.on = true;
+  rollout_status r = rollout_decode_step(ctx, d_tokens, d_logits);
+  ctx->prof.on = false;
+  if (r) return r;
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream), "stream sync");
+  std::memset(out, 0, sizeof(*out));
+  for (const Prof::Rec& rec : ctx->prof.recs) {
+    float ms = 0.f;
+    HIP_TRY(ctx, hipEventElapsedTime(&ms, ctx->prof.ev[rec.e0], ctx->prof.ev[rec.e1]), "event time");
+    out->ms[rec.cls] += ms;
+    out->launches[rec.cls] += 1;
+    out->bytes[rec.cls] += rec.bytes;
+    out->flops[rec.cls] += rec.flops;
+  }
+  return ROLLOUT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,114 @@
+"""The C ABI on the CPU: every declared symbol is exported, the planner's
+arithmetic, and argument validation that runs before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_11226_amd as R
+from conftest import ROOT
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "rollout.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rollout_\w+|grpo_\w+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 12
+    lib = ctypes.CDLL(R.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(R.EXPORTED) == names
+
+
+def _cfg(shape="7b", dtype=1, P=256, N=512, S=64, budget=288 * 10**9, **kw):
+    return R.model_config(shape, dtype, P, N, S, hbm_budget_bytes=budget, **kw)
+
+
+def test_plan_weight_bytes_match_the_shapes():
+    # parameter counts of the dense decoders (untied head, no biases), 2 bytes each in bf16
+    for shape, params in (("7b", 7_615_487_488), ("14b", 14_769_689_600), ("72b", 72_705_384_448)):
+        p = R.rollout_plan(_cfg(shape), 8)
+        norms = (2 * R.SHAPES[shape][0] + 1) * R.SHAPES[shape][1]
+        matrices = params - norms
+        # each tensor is aligned to 256 bytes; norms are fp32
+        assert 0 <= p.weight_bytes - (2 * matrices + 4 * norms) < 256 * (6 * R.SHAPES[shape][0] + 4)
+
+
+def test_plan_kv_blocks_share_prompt_blocks():
+    P, N, G, S = 256, 512, 8, 64
+    p = R.rollout_plan(_cfg(P=P, N=N, S=S), G)
+    assert p.seqs_in_flight_max == S
+    # per group: P/16 shared blocks + G * (ceil((P+N)/16) - P/16) private blocks
+    assert p.kv_blocks == (S // G) * (P // 16 + G * ((P + N) // 16 - P // 16))
+    assert p.kv_block_bytes == 28 * 4 * 2 * 16 * 128 * 2
+    assert p.arena_bytes >= p.weight_bytes + p.kv_bytes
+
+
+def test_plan_snaps_to_whole_groups():
+    for G in (3, 5, 7, 8, 64):
+        p = R.rollout_plan(_cfg(S=100), G)
+        assert p.seqs_in_flight_max % G == 0 and p.seqs_in_flight_max <= 100
+        assert p.seqs_in_flight_max == 100 // G * G
+
+
+def test_plan_budget_limits_concurrency():
+    big = R.rollout_plan(_cfg("14b", P=512, N=1024, S=2048), 16)
+    assert big.seqs_in_flight_max < 2048 and big.arena_bytes <= 288 * 10**9
+    # one more group would not have fit
+    small = R.rollout_plan(_cfg("14b", P=512, N=1024, S=big.seqs_in_flight_max + 16, budget=big.arena_bytes), 16)
+    assert small.seqs_in_flight_max == big.seqs_in_flight_max
+
+
+def test_plan_errors():
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_plan(_cfg(budget=10**9), 8)  # weights alone exceed the budget
+    assert e.value.code == R.ENOMEM
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_plan(_cfg(), 0)
+    assert e.value.code == R.EINVAL
+    bad = _cfg()
+    bad.head_dim = 48
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_plan(bad, 1)
+    assert e.value.code == R.EUNSUPPORTED
+    bad = _cfg()
+    bad.n_kv_heads = 3
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_plan(bad, 1)
+    assert e.value.code == R.EUNSUPPORTED
+    bad = _cfg()
+    bad.dtype = 7
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_plan(bad, 1)
+    assert e.value.code == R.EINVAL
+    assert "dtype" in R.rollout_last_error()
+
+
+def test_validation_before_device_work():
+    # these return before touching the device, so they run without a GPU
+    with pytest.raises(R.RolloutError) as e:
+        R.grpo_advantages(None, 4, 8, 0.0, 1, None)
+    assert e.value.code == R.EINVAL
+    with pytest.raises(R.RolloutError) as e:
+        R.grpo_advantages(0x1000, 4, 8, 0.0, 2, 0x2000)
+    assert e.value.code == R.EINVAL
+    with pytest.raises(R.RolloutError) as e:
+        R.grpo_advantages(0x1000, 0, 8, 0.0, 1, 0x2000)
+    assert e.value.code == R.EINVAL
+    for fn, args in ((R.rollout_prefill, (0x1000, 1, 4, 1, 0x2000)), (R.rollout_decode_step, (0x1000, 0x2000)),
+                     (R.rollout_sample, (0x1000, 1, 1.0, 1.0, 0x2000, 0x3000)), (R.rollout_sync, ())):
+        with pytest.raises(R.RolloutError) as e:
+            fn(None, *args)
+        assert e.value.code == R.EINVAL
+    cfg = _cfg()
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_init(cfg, 0x1000, 1024)  # far too small an arena
+    assert e.value.code == R.ENOMEM
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_init(cfg, 0x1001, 10**12)  # misaligned
+    assert e.value.code == R.EINVAL
