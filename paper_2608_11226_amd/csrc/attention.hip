@@ -1,19 +1,35 @@
 // Paged grouped-query attention over the KV cache, split over the context.
 //
-// One workgroup per (row, KV head, context split).  All query heads that share
-// the KV head (n_heads / n_kv_heads of them) are served by the same workgroup,
-// so every K/V tile is read from HBM once per row and reused from LDS by the
-// whole group.  Scores use the 1/sqrt(hd) scale; the softmax is the online
-// (running max / running sum) form, and each split leaves an unnormalised
-// output with its (max, sum) for the combine kernel, which merges the splits
-// by log-sum-exp weights in split order.
+// Every query row attends to keys 0 .. pos of its sequence (causal), with the
+// 1/sqrt(hd) scale and a max-subtracted softmax.  The context is cut into
+// splits; each split leaves an unnormalised output with its running (max, sum)
+// and the combine kernel merges the splits with log-sum-exp weights, in split
+// order.
 //
-// Cache layout (per block of `blk` tokens): [block][layer][kv head][K|V][blk][hd].
-// A row sees keys 0 .. pos (causal): pos is its position in the sequence.
+// bf16 path, head_dim 64 or 128: one wavefront per (row, KV head, split).  All
+// query heads of the KV head's group ride in one MFMA (up to 16 heads): with
+// the scores computed transposed, S^T = K Q^T (16 tokens x 16 heads per
+// v_mfma_f32_16x16x32_bf16 step over hd), each lane holds the scores of one
+// head for four tokens, which is exactly the B-operand layout of the P V
+// product, so O^T = V^T P^T (v_mfma_f32_16x16x16_bf16, one per 16 output
+// dimensions) consumes the softmaxed tile straight from registers.  Softmax
+// statistics need only two cross-lane shuffles per 16-token tile.  K and V
+// tiles are read once per row and KV head, two 16-token tiles in flight per
+// wave.  P is rounded to bf16 for the MFMA (scores, softmax and accumulation
+// are fp32).
+//
+// fp32 path (and head_dim 32): a VALU kernel with the same split structure
+// that stages K/V tiles in LDS.
+//
+// Cache block layout: [block][layer][kv head][K: blk x hd | V: hd x blk].
 #include "internal.h"
 
 namespace rollout {
 namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int* pos) {
   if (rm.P > 0) {
@@ -26,11 +42,156 @@ __device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int
   }
 }
 
+__device__ __forceinline__ short f2bs(float f) { return (short)f32_to_bf16(f); }
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
+                                                   const uint16_t* __restrict__ kv, int n_blocks,
+                                                   const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
+                                                   int R, int splits, int split_tokens, int layer,
+                                                   float* __restrict__ opart, float* __restrict__ ml,
+                                                   int32_t* __restrict__ err) {
+  constexpr int KC = HD / 32;  // QK^T k-steps
+  constexpr int DT = HD / 16;  // P.V output tiles
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= R * D.nkv * splits) return;  // no barriers below
+  const int split = item % splits;
+  const int kvh = (item / splits) % D.nkv;
+  const int r = item / (splits * D.nkv);
+  int seq, pos;
+  row_place(rm, r, &seq, &pos);
+  const int t_begin = split * split_tokens;
+  const int t_end = min(pos + 1, t_begin + split_tokens);
+  const int nrep = D.nh / D.nkv;
+  const int hh = lane & 15, g = lane >> 4;
+  const int blk = D.blk;
+  const size_t blk_elems = (size_t)blk * HD;
+  const size_t kv_head_stride = 2 * blk_elems;
+  const size_t layer_base = ((size_t)layer * D.nkv + kvh) * kv_head_stride;
+  const size_t block_stride = (size_t)D.L * D.nkv * kv_head_stride;
+  const int32_t* trow = tables + (size_t)seq * max_blocks;
+
+  bf16x8_t zero8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
+  const short4_t zero4 = {0, 0, 0, 0};
+
+  // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
+  bf16x8_t qf[KC];
+  {
+    const uint16_t* qrow = q + (size_t)r * D.qd + (size_t)(kvh * nrep + hh) * HD;
+#pragma unroll
+    for (int c = 0; c < KC; ++c)
+      qf[c] = hh < nrep ? *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c + 8 * g) : zero8;
+  }
+  const float scale = 1.0f / sqrtf((float)HD);
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx4_t o[DT];
+#pragma unroll
+  for (int j = 0; j < DT; ++j) o[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int t0 = t_begin; t0 < t_end; t0 += 32) {
+    // loads of two 16-token tiles first, so both are in flight together
+    bf16x8_t kf[2][KC];
+    short4_t vf[2][DT];
+    int vmask[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int tb = t0 + 16 * u;
+      const int tk = tb + hh;  // key row supplied by this lane
+      if (tk < t_end) {
+        const int b = trow[tk / blk];
+        if (b >= 0 && b < n_blocks) {
+          const uint16_t* kp = kv + (size_t)b * block_stride + layer_base + (size_t)(tk % blk) * HD + 8 * g;
+#pragma unroll
+          for (int c = 0; c < KC; ++c) kf[u][c] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * c);
+        } else {
+          atomicOr(err, 4);
+#pragma unroll
+          for (int c = 0; c < KC; ++c) kf[u][c] = zero8;
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < KC; ++c) kf[u][c] = zero8;
+      }
+      const int tv = tb + 4 * g;  // four value tokens tv .. tv+3 (never straddle a block)
+      vmask[u] = tv < t_end ? min(4, t_end - tv) : 0;
+      if (vmask[u] > 0) {
+        const int b = trow[tv / blk];
+        if (b >= 0 && b < n_blocks) {
+          const uint16_t* vp = kv + (size_t)b * block_stride + layer_base + blk_elems + (tv % blk);
+#pragma unroll
+          for (int j = 0; j < DT; ++j) vf[u][j] = *reinterpret_cast<const short4_t*>(vp + (size_t)(16 * j + hh) * blk);
+        } else {
+          vmask[u] = 0;
+        }
+      }
+      if (vmask[u] < 4) {  // tokens past the context may hold stale data: never let them reach the MFMA
+#pragma unroll
+        for (int j = 0; j < DT; ++j) {
+          if (vmask[u] == 0) vf[u][j] = zero4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (e >= vmask[u]) vf[u][j][e] = 0;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int tb = t0 + 16 * u;
+      if (tb >= t_end) break;
+      floatx4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < KC; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[c], s, 0, 0, 0);
+      // s[i] = score of token tb + 4g + i for head hh
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[i] = (tb + 4 * g + i < t_end) ? s[i] * scale : -INFINITY;
+        mx = fmaxf(mx, s[i]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
+      float p[4], ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p[i] = (s[i] == -INFINITY) ? 0.f : expf(s[i] - m_new);
+        ps += p[i];
+      }
+      ps += __shfl_xor(ps, 16, 64);
+      ps += __shfl_xor(ps, 32, 64);
+      l_run = l_run * alpha + ps;
+      m_run = m_new;
+      const short4_t pf = {f2bs(p[0]), f2bs(p[1]), f2bs(p[2]), f2bs(p[3])};
+#pragma unroll
+      for (int j = 0; j < DT; ++j) {
+        o[j] *= alpha;
+        o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf[u][j], pf, o[j], 0, 0, 0);
+      }
+    }
+  }
+  // o[j][i] = unnormalised output of head hh at dimension 16 j + 4 g + i
+  if (hh < nrep) {
+    float* op = opart + (((size_t)r * D.nh + kvh * nrep + hh) * splits + split) * HD + 4 * g;
+#pragma unroll
+    for (int j = 0; j < DT; ++j) *reinterpret_cast<float4*>(op + 16 * j) = make_float4(o[j][0], o[j][1], o[j][2], o[j][3]);
+    if (g == 0) {
+      float* mp = ml + (((size_t)r * D.nh + kvh * nrep + hh) * splits + split) * 2;
+      mp[0] = m_run;
+      mp[1] = l_run;
+    }
+  }
+}
+
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void k_attn(Dims D, const T* __restrict__ q, const T* __restrict__ kv, int n_blocks,
-                                              const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
-                                              int splits, int split_tokens, int layer, float* __restrict__ opart,
-                                              float* __restrict__ ml, int32_t* __restrict__ err) {
+__global__ __launch_bounds__(256) void k_attn_valu(Dims D, const T* __restrict__ q, const T* __restrict__ kv,
+                                                   int n_blocks, const int32_t* __restrict__ tables, int max_blocks,
+                                                   RowMap rm, int splits, int split_tokens, int layer,
+                                                   float* __restrict__ opart, float* __restrict__ ml,
+                                                   int32_t* __restrict__ err) {
   constexpr int TT = 32;
   constexpr int NACC = 16 * HD / 256;
   __shared__ float qs[16][HD];
@@ -45,10 +206,9 @@ __global__ __launch_bounds__(256) void k_attn(Dims D, const T* __restrict__ q, c
   const int r = blockIdx.x / (splits * D.nkv);
   int seq, pos;
   row_place(rm, r, &seq, &pos);
-  const int ctx = pos + 1;
   const int nrep = D.nh / D.nkv;
   const int t_begin = split * split_tokens;
-  const int t_end = min(ctx, t_begin + split_tokens);
+  const int t_end = min(pos + 1, t_begin + split_tokens);
   const float scale = 1.0f / sqrtf((float)HD);
   const size_t blk_elems = (size_t)D.blk * HD;
 
@@ -70,9 +230,9 @@ __global__ __launch_bounds__(256) void k_attn(Dims D, const T* __restrict__ q, c
       const int b = tables[(size_t)seq * max_blocks + tok / D.blk];
       float kval = 0.f, vval = 0.f;
       if (b >= 0 && b < n_blocks) {
-        const size_t base = (((size_t)b * D.L + layer) * D.nkv + kvh) * 2 * blk_elems + (size_t)(tok % D.blk) * HD + dd;
-        kval = ldf(kv, base);
-        vval = ldf(kv, base + blk_elems);
+        const size_t base = (((size_t)b * D.L + layer) * D.nkv + kvh) * 2 * blk_elems;
+        kval = ldf(kv, base + (size_t)(tok % D.blk) * HD + dd);
+        vval = ldf(kv, base + blk_elems + (size_t)dd * D.blk + (tok % D.blk));
       } else if (dd == 0) {
         atomicOr(err, 4);
       }
@@ -133,32 +293,41 @@ __global__ __launch_bounds__(256) void k_attn(Dims D, const T* __restrict__ q, c
   }
 }
 
+// out (O-projection operand layout) = sum_s w_s o_s / sum_s w_s l_s, w_s = exp(m_s - max m)
 template <typename T>
-__global__ void k_attn_combine(const float* __restrict__ opart, const float* __restrict__ ml, int splits, int hd,
-                               T* __restrict__ out) {
-  const size_t rh = blockIdx.x;  // row * n_heads + head
-  const int d = threadIdx.x;
+__global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ opart, const float* __restrict__ ml,
+                                                     int R, int nh, int splits, int hd, T* __restrict__ out) {
+  const int r = blockIdx.x;
+  const int g = blockIdx.y * 64 + threadIdx.x;  // group of 8 output columns
+  const int qd = nh * hd;
+  if (g >= (qd >> 3)) return;
+  const int h = (g * 8) / hd, d0 = (g * 8) % hd;
+  const size_t rh = (size_t)r * nh + h;
   float mx = -INFINITY;
-  for (int s = 0; s < splits; ++s) {
-    const float l = ml[(rh * splits + s) * 2 + 1];
-    if (l > 0.f) mx = fmaxf(mx, ml[(rh * splits + s) * 2]);
-  }
-  float num = 0.f, den = 0.f;
+  for (int s = 0; s < splits; ++s)
+    if (ml[(rh * splits + s) * 2 + 1] > 0.f) mx = fmaxf(mx, ml[(rh * splits + s) * 2]);
+  float num[8] = {0, 0, 0, 0, 0, 0, 0, 0}, den = 0.f;
   for (int s = 0; s < splits; ++s) {
     const float m = ml[(rh * splits + s) * 2], l = ml[(rh * splits + s) * 2 + 1];
     if (l > 0.f) {
       const float w = expf(m - mx);
-      num += w * opart[(rh * splits + s) * hd + d];
+      float v[8];
+      ld8(opart, (rh * splits + s) * hd + d0, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) num[e] += w * v[e];
       den += w * l;
     }
   }
-  stf(out, rh * hd + d, den > 0.f ? num / den : 0.f);
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = den > 0.f ? num[e] / den : 0.f;
+  st8(out, xoff(out, r, g * 8, qd, (R + 15) >> 4), o);
 }
 
 }  // namespace
 
 int attn_splits(int max_ctx, int* split_tokens) {
-  const int st = 256;
+  const int st = 128;
   *split_tokens = st;
   const int s = (max_ctx + st - 1) / st;
   return s < 1 ? 1 : s;
@@ -168,14 +337,23 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const v
                             const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
                             int layer, float* opart, float* ml, int32_t* err) {
   if (R <= 0) return hipSuccess;
+  if (D.dtype == ROLLOUT_DTYPE_BF16 && (D.hd == 128 || D.hd == 64)) {
+    const int items = R * D.nkv * splits;
+    const dim3 grid((items + 3) / 4);
+    if (D.hd == 128)
+      hipLaunchKernelGGL(k_attn_mfma<128>, grid, dim3(256), 0, s, D, (const uint16_t*)q, (const uint16_t*)kv_pool,
+                         n_blocks, tables, max_blocks, rm, R, splits, split_tokens, layer, opart, ml, err);
+    else
+      hipLaunchKernelGGL(k_attn_mfma<64>, grid, dim3(256), 0, s, D, (const uint16_t*)q, (const uint16_t*)kv_pool,
+                         n_blocks, tables, max_blocks, rm, R, splits, split_tokens, layer, opart, ml, err);
+    return hipGetLastError();
+  }
   const dim3 grid((unsigned)R * D.nkv * splits);
-#define ROLLOUT_ATTN(T, HD)                                                                                   \
-  hipLaunchKernelGGL((k_attn<T, HD>), grid, dim3(256), 0, s, D, (const T*)q, (const T*)kv_pool, n_blocks, tables, \
+#define ROLLOUT_ATTN(T, HD)                                                                                        \
+  hipLaunchKernelGGL((k_attn_valu<T, HD>), grid, dim3(256), 0, s, D, (const T*)q, (const T*)kv_pool, n_blocks, tables, \
                      max_blocks, rm, splits, split_tokens, layer, opart, ml, err)
   if (D.dtype == ROLLOUT_DTYPE_BF16) {
-    if (D.hd == 128) ROLLOUT_ATTN(uint16_t, 128);
-    else if (D.hd == 64) ROLLOUT_ATTN(uint16_t, 64);
-    else ROLLOUT_ATTN(uint16_t, 32);
+    ROLLOUT_ATTN(uint16_t, 32);
   } else {
     if (D.hd == 128) ROLLOUT_ATTN(float, 128);
     else if (D.hd == 64) ROLLOUT_ATTN(float, 64);
@@ -188,11 +366,12 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const v
 hipError_t launch_attn_combine(hipStream_t s, const Dims& D, const float* opart, const float* ml, int R, int splits,
                                void* out) {
   if (R <= 0) return hipSuccess;
-  const dim3 grid((unsigned)R * D.nh);
+  const dim3 grid(R, ((D.qd >> 3) + 63) / 64);
   if (D.dtype == ROLLOUT_DTYPE_BF16)
-    hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(D.hd), 0, s, opart, ml, splits, D.hd, (uint16_t*)out);
+    hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(64), 0, s, opart, ml, R, D.nh, splits, D.hd,
+                       (uint16_t*)out);
   else
-    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(D.hd), 0, s, opart, ml, splits, D.hd, (float*)out);
+    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(64), 0, s, opart, ml, R, D.nh, splits, D.hd, (float*)out);
   return hipGetLastError();
 }
 

@@ -1,22 +1,26 @@
 // Projection GEMMs: out[split][m][n] = sum_{k in split} X[m][k] * W[n][k], fp32 result.
 //
-// bf16 path (CDNA4 MFMA, v_mfma_f32_16x16x32_bf16).  The weight matrix is the
-// MFMA A operand: it is stored pre-tiled in operand order (16 rows x 32 k per
-// 1 KiB tile, lane-major), so one wave reads one tile with a single fully
-// coalesced 16-byte-per-lane load and weights stream from HBM exactly once.
-// The activations X (bf16, row-major) are the B operand; each workgroup stages
-// a [M_tile x KC] slab of X in LDS, in operand order, and its four waves (one
-// 16-row weight block each) reuse it.  Weights for the next K chunk are loaded
-// into registers while the MFMAs of the current chunk run.  Small-N
-// projections are split over K so a launch has enough workgroups to keep every
-// CU streaming; the split partials are summed in a fixed order by the
-// epilogue kernels, so results are deterministic.
+// bf16 path (CDNA4 MFMA, v_mfma_f32_16x16x32_bf16).  Both operands live in
+// HBM in MFMA operand order, so every global load is a fully coalesced
+// 16-byte-per-lane read and every LDS access is conflict-free:
+//   W (A operand): tiles of 16 weight rows x 32 k, [N/16][K/32][64 lanes][8],
+//                  lane = row%16 + 16*((k%32)/8) -- written once at synthesis;
+//   X (B operand): tiles of 32 k x 16 activation rows, [K/32][M/16][64][8],
+//                  lane = m%16 + 16*((k%32)/8) -- written by the producing
+//                  kernel (norm, SwiGLU, attention combine).
+// A workgroup of four waves owns 64 weight rows (16 per wave) and a K range;
+// it stages X for the range through a double-buffered LDS slab shared by the
+// four waves, while the weights (read exactly once) and the next X slab are
+// already in flight in registers.  Projections with few output rows are split
+// over K so that every CU streams weights; split partials are summed in split
+// order by the consuming kernel, so results are deterministic.
 //
-// fp32 path: a plain LDS-tiled VALU GEMM (the fp32 path exists for exact
-// parity on small models, not for speed).
-#include "internal.h"
-
+// fp32 path: a plain LDS-tiled VALU GEMM over row-major X and W (the fp32
+// path exists for exact parity on small models, not for speed).
 #include <algorithm>
+#include <cstdlib>
+
+#include "internal.h"
 
 namespace rollout {
 namespace {
@@ -24,74 +28,87 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
-template <int MB, int KC>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X, int ldx,
-                                                   const uint16_t* __restrict__ W, float* __restrict__ out, int M,
-                                                   int N, int K, int kslice) {
-  constexpr int KS = KC / 32;
-  __shared__ bf16x8_t xs[KS][MB][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+template <int MB, int KS>
+__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
+                                                   float* __restrict__ out, int M, int N, int K, int kslice) {
+  constexpr int XV = KS * MB * 64;  // 16-byte X vectors per chunk
+  constexpr int XPT = (XV + 255) / 256;
+  __shared__ bf16x8_t xs[2][XV];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nb = blockIdx.x * 4 + wave;
   const bool nvalid = nb * 16 < N;
-  const int kbt = K / 32;
-  const int k0 = blockIdx.y * kslice;
-  const int k1 = min(K, k0 + kslice);
-  const int m0 = blockIdx.z * (MB * 16);
-  const bf16x8_t* wp = reinterpret_cast<const bf16x8_t*>(W) + (size_t)(nvalid ? nb : 0) * (size_t)kbt * 64 + lane;
+  const int kbt = K >> 5;
+  const int Mb = (M + 15) >> 4;
+  const int kb0 = (int)(blockIdx.y * kslice) >> 5;
+  const int kb1 = min(kbt, kb0 + (kslice >> 5));
+  const int mb0 = blockIdx.z * MB;
+  const bf16x8_t* wp = W + (size_t)(nvalid ? nb : 0) * (size_t)kbt * 64 + lane;
 
   bf16x8_t zero;
 #pragma unroll
   for (int e = 0; e < 8; ++e) zero[e] = (__bf16)0.0f;
-
   floatx4_t acc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  bf16x8_t wcur[KS], wnxt[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    wcur[ks] = (nvalid && k0 + ks * 32 < k1) ? wp[(size_t)(k0 / 32 + ks) * 64] : zero;
-    wnxt[ks] = zero;
+  bf16x8_t wcur[KS], wnxt[KS], xr[XPT];
+#define LOAD_W(dst, kb)                                                                \
+  _Pragma("unroll") for (int ks = 0; ks < KS; ++ks) dst[ks] =                          \
+      (nvalid && (kb) + ks < kb1) ? wp[(size_t)((kb) + ks) * 64] : zero;
+#define LOAD_X(kb)                                                                      \
+  _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
+    const int v = tid + 256 * j;                                                        \
+    bf16x8_t t = zero;                                                                  \
+    if (v < XV) {                                                                       \
+      const int ks = v / (MB * 64), mb = (v >> 6) % MB, ln = v & 63;                    \
+      const int m = (mb0 + mb) * 16 + (ln & 15), kk = (kb) + ks;                        \
+      if (kk < kb1 && m < M) t = XF[((size_t)kk * Mb + mb0 + mb) * 64 + ln];            \
+    }                                                                                   \
+    xr[j] = t;                                                                          \
+  }
+#define STORE_X(buf)                                                                    \
+  _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
+    const int v = tid + 256 * j;                                                        \
+    if (v < XV) xs[buf][v] = xr[j];                                                     \
   }
 
-  for (int kc = k0; kc < k1; kc += KC) {
-    const int nks = min(KS, (k1 - kc) / 32);
-    // stage X[m0 .. m0 + 16 MB) x [kc, kc + 32 nks) into LDS in B-operand order
-    const int items = MB * 16 * nks * 4;
-    for (int it = threadIdx.x; it < items; it += 256) {
-      const int kq = it & 3;
-      const int rest = it >> 2;
-      const int ks = rest % nks;
-      const int ml = rest / nks;
-      const int m = m0 + ml;
-      bf16x8_t v = zero;
-      if (m < M) v = *reinterpret_cast<const bf16x8_t*>(X + (size_t)m * ldx + kc + ks * 32 + kq * 8);
-      xs[ks][ml >> 4][(ml & 15) + 16 * kq] = v;
+  LOAD_W(wcur, kb0);
+  LOAD_X(kb0);
+  STORE_X(0);
+  __syncthreads();
+  int buf = 0;
+  for (int kb = kb0; kb < kb1; kb += KS) {
+    const int kn = kb + KS;
+    const bool more = kn < kb1;
+    if (more) {
+      LOAD_W(wnxt, kn);
+      LOAD_X(kn);
     }
-    __syncthreads();
-    const int kn = kc + KC;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      if (nvalid && kn + ks * 32 < k1) wnxt[ks] = wp[(size_t)(kn / 32 + ks) * 64];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      if (ks < nks) {
+      if (kb + ks < kb1) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
-          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks], xs[ks][mb][lane], acc[mb], 0, 0, 0);
+          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks], xs[buf][(ks * MB + mb) * 64 + lane], acc[mb],
+                                                            0, 0, 0);
       }
     }
+    if (more) STORE_X(buf ^ 1);
     __syncthreads();
+    buf ^= 1;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) wcur[ks] = wnxt[ks];
   }
+#undef LOAD_W
+#undef LOAD_X
+#undef STORE_X
   if (!nvalid) return;
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
   float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
   const int n = nb * 16 + 4 * (lane >> 4);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
-    const int m = m0 + mb * 16 + (lane & 15);
+    const int m = (mb0 + mb) * 16 + (lane & 15);
     if (m < M)
       *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]);
   }
@@ -120,12 +137,17 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   if (m < M && n < N) out[(size_t)m * N + n] = acc;
 }
 
+// m-blocks of 16 rows handled by one workgroup pass
 int mb_for(int M) {
-  if (M <= 16) return 1;
-  if (M <= 32) return 2;
-  if (M <= 64) return 4;
-  if (M <= 128) return 8;
+  const int mb = (M + 15) / 16;
+  if (mb <= 4) return mb;
+  if (mb <= 8) return 8;
   return 16;
+}
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  return v ? std::atoi(v) : dflt;
 }
 
 int kslice_for(int K, int splits) {
@@ -137,12 +159,13 @@ int kslice_for(int K, int splits) {
 
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;
+  static const int target = env_int("ROLLOUT_GEMM_TARGET_WG", 512);
+  static const int min_k = env_int("ROLLOUT_GEMM_MIN_KSLICE", 512);
   const int mb = mb_for(M);
-  const int mchunks = (M + mb * 16 - 1) / (mb * 16);
+  const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
   const int nwg = (N + 63) / 64 * mchunks;
-  const int target = 1024;  // about four workgroups per CU
   int s = (target + nwg - 1) / nwg;
-  s = std::min(s, std::max(1, K / 256));
+  s = std::min(s, std::max(1, K / min_k));
   s = std::min(s, max_splits);
   s = std::max(s, 1);
   const int ks = kslice_for(K, s);
@@ -159,15 +182,17 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
   }
   const int mb = mb_for(M);
   const int kslice = kslice_for(K, splits);
-  dim3 grid((N + 63) / 64, splits, (M + mb * 16 - 1) / (mb * 16));
-  const uint16_t* x = (const uint16_t*)X;
-  const uint16_t* w = (const uint16_t*)W;
+  const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
+  dim3 grid((N + 63) / 64, splits, mchunks);
+  const bf16x8_t* x = (const bf16x8_t*)X;
+  const bf16x8_t* w = (const bf16x8_t*)W;
   switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 256>), grid, dim3(256), 0, s, x, ldx, w, out, M, N, K, kslice); break;
-    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 256>), grid, dim3(256), 0, s, x, ldx, w, out, M, N, K, kslice); break;
-    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 256>), grid, dim3(256), 0, s, x, ldx, w, out, M, N, K, kslice); break;
-    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 256>), grid, dim3(256), 0, s, x, ldx, w, out, M, N, K, kslice); break;
-    default: hipLaunchKernelGGL((k_gemm_bf16<16, 128>), grid, dim3(256), 0, s, x, ldx, w, out, M, N, K, kslice); break;
+    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
+    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
+    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
+    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
+    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 4>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
+    default: hipLaunchKernelGGL((k_gemm_bf16<16, 2>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
   }
   return hipGetLastError();
 }

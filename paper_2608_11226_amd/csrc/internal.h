@@ -116,6 +116,46 @@ __device__ __forceinline__ float ldf(const uint16_t* p, size_t i) { return bf16_
 __device__ __forceinline__ void stf(float* p, size_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void stf(uint16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
 
+// Element (m, k) of an M x K GEMM activation operand.  bf16 operands are kept
+// in MFMA B-operand order, tiles of 32 k x 16 rows: [K/32][Mb][64 lanes][8],
+// lane = m%16 + 16*((k%32)/8), Mb = ceil(M/16); fp32 operands are row-major.
+// Eight consecutive k starting at a multiple of 8 are contiguous in both.
+__device__ __forceinline__ size_t xoff(const uint16_t*, int m, int k, int K, int Mb) {
+  (void)K;
+  return ((size_t)((k >> 5) * Mb + (m >> 4)) * 64 + (size_t)((m & 15) + ((k & 31) >> 3) * 16)) * 8 + (k & 7);
+}
+__device__ __forceinline__ size_t xoff(const float*, int m, int k, int K, int Mb) {
+  (void)Mb;
+  return (size_t)m * K + k;
+}
+
+// Eight consecutive values at element index i (i a multiple of 8).
+__device__ __forceinline__ void st8(float* p, size_t i, const float* v) {
+  reinterpret_cast<float4*>(p + i)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p + i)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void st8(uint16_t* p, size_t i, const float* v) {
+  uint4 u;
+  u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+  u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+  u.z = (uint32_t)f32_to_bf16(v[4]) | ((uint32_t)f32_to_bf16(v[5]) << 16);
+  u.w = (uint32_t)f32_to_bf16(v[6]) | ((uint32_t)f32_to_bf16(v[7]) << 16);
+  *reinterpret_cast<uint4*>(p + i) = u;
+}
+__device__ __forceinline__ void ld8(const float* p, size_t i, float* v) {
+  const float4 a = reinterpret_cast<const float4*>(p + i)[0], b = reinterpret_cast<const float4*>(p + i)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void ld8(const uint16_t* p, size_t i, float* v) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p + i);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = __uint_as_float(w[j] << 16);
+    v[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+  }
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -4,8 +4,13 @@
 //
 // Every kernel that consumes GEMM partials sums the K splits in split order,
 // so the result does not depend on scheduling.  The residual stream is fp32;
-// the outputs that feed a GEMM, and the cached K/V, are written in the cache
-// dtype (bf16, rounded to nearest-even, on the bf16 path).
+// the outputs that feed a GEMM are written in the GEMM's operand layout
+// (xoff) and, like the cached K/V, in the cache dtype (bf16 rounded to
+// nearest-even on the bf16 path).
+//
+// Cache block layout (blk tokens): [block][layer][kv head][K: blk x hd | V: hd x blk];
+// K is token-major, V is dimension-major so the attention kernel's P.V MFMA
+// reads four consecutive tokens of one dimension as one 8-byte load.
 #include "internal.h"
 
 namespace rollout {
@@ -25,133 +30,156 @@ __global__ __launch_bounds__(256) void k_embed(const T* __restrict__ E, const in
   for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)m * d + i] = ldf(E, (size_t)tok * d + i);
 }
 
-// x[m] += sum_s part[s][m]; out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * gain
+// x[m] += sum_s part[s][m]; out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * gain  (GEMM operand layout)
 template <typename T>
 __global__ __launch_bounds__(256) void k_residual_norm(const float* __restrict__ part, int splits, int M, int d,
                                                        float* __restrict__ x, const float* __restrict__ gain,
                                                        float eps, T* __restrict__ out) {
   __shared__ float red[32];
   const int m = blockIdx.x;
+  const int Mb = (M + 15) >> 4;
   float* xr = x + (size_t)m * d;
+  const int ng = d >> 3;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    float v = xr[i];
+  for (int g = threadIdx.x; g < ng; g += blockDim.x) {
+    float v[8];
+    ld8(xr, (size_t)g * 8, v);
     if (part) {
-      float acc = 0.f;
-      for (int s = 0; s < splits; ++s) acc += part[((size_t)s * M + m) * d + i];
-      v += acc;
-      xr[i] = v;
+      for (int s = 0; s < splits; ++s) {
+        float p[8];
+        ld8(part, ((size_t)s * M + m) * d + (size_t)g * 8, p);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += p[e];
+      }
+      st8(xr, (size_t)g * 8, v);
     }
-    ss += v * v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
   }
   const float tot = block_sum(ss, red);
   const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x) stf(out, (size_t)m * d + i, xr[i] * r * gain[i]);
+  for (int g = threadIdx.x; g < ng; g += blockDim.x) {
+    float v[8], gn[8];
+    ld8(xr, (size_t)g * 8, v);
+    ld8(gain, (size_t)g * 8, gn);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * r * gn[e];
+    st8(out, xoff(out, m, g * 8, d, Mb), v);
+  }
 }
 
-__device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int* pos, int* copies) {
+__device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int* pos) {
   if (rm.P > 0) {
     const int p = m / rm.P;
     *pos = m - p * rm.P;
     *seq = rm.seq0 + p * rm.G;
-    *copies = 1;
   } else {
     *seq = rm.seq0 + m;
     *pos = rm.ctx_len[m];
-    *copies = 1;
   }
 }
 
-// One block per row: sum the K splits of [q | k | v], rotate q and k
-// (rotate-half pairs (i, i + hd/2), angle table cos/sin[pos][i]), write q in
-// the cache dtype and append k and v to the paged cache at the row's position.
+// One wave per (row, head slot): slots [0, nh) are query heads, [nh, nh+nkv)
+// key heads, [nh+nkv, nh+2nkv) value heads; slot s owns columns [s*hd, s*hd+hd)
+// of the fused QKV output.  Query and key heads are rotated (rotate-half pairs
+// (i, i + hd/2), angles cos/sin[pos][i]); keys and values are appended to the
+// paged cache at the row's position.
 template <typename T>
-__global__ __launch_bounds__(256) void k_qkv_epilogue(Dims D, const float* __restrict__ part, int splits, int M,
-                                                      RowMap rm, const float* __restrict__ rcos,
-                                                      const float* __restrict__ rsin, T* __restrict__ q_out,
-                                                      T* __restrict__ kv, int n_blocks,
-                                                      const int32_t* __restrict__ tables, int max_blocks, int layer,
-                                                      int32_t* __restrict__ err) {
-  const int m = blockIdx.x;
-  int seq, pos, copies;
-  row_place(rm, m, &seq, &pos, &copies);
+__global__ __launch_bounds__(64) void k_qkv_epilogue(Dims D, const float* __restrict__ part, int splits, int M,
+                                                     RowMap rm, const float* __restrict__ rcos,
+                                                     const float* __restrict__ rsin, T* __restrict__ q_out,
+                                                     T* __restrict__ kv, int n_blocks,
+                                                     const int32_t* __restrict__ tables, int max_blocks, int layer,
+                                                     int32_t* __restrict__ err) {
+  const int m = blockIdx.x, slot = blockIdx.y, tid = threadIdx.x;
+  int seq, pos;
+  row_place(rm, m, &seq, &pos);
   const int hd = D.hd, half = hd / 2;
   // prefill rows in the last, partly filled prompt block go to every sequence of the group
-  if (rm.P > 0 && (pos / D.blk) * D.blk + D.blk > rm.P) copies = rm.G;
+  const int copies = (rm.P > 0 && (pos / D.blk) * D.blk + D.blk > rm.P) ? rm.G : 1;
   const int n = D.nqkv;
-  const float* pr = part + (size_t)m * n;
   const size_t split_stride = (size_t)M * n;
-  auto val = [&](int c) {
-    float a = 0.f;
-    for (int s = 0; s < splits; ++s) a += pr[s * split_stride + c];
-    return a;
-  };
-  const float* cs = rcos + (size_t)pos * half;
-  const float* sn = rsin + (size_t)pos * half;
-  const int nrot = (D.nh + D.nkv) * half;  // rotated pairs of q and k heads
+  const float* pr = part + (size_t)m * n + (size_t)slot * hd;
   const size_t blk_elems = (size_t)D.blk * hd;
-  for (int j = threadIdx.x; j < nrot + D.kvd; j += blockDim.x) {
-    if (j < nrot) {
-      const int h = j / half, i = j - h * half;  // q heads first, then k heads
-      const int c0 = h * hd + i;
-      const float x1 = val(c0), x2 = val(c0 + half);
+  const int kslot = slot - D.nh, vslot = slot - D.nh - D.nkv;
+  if (vslot < 0) {
+    const float* cs = rcos + (size_t)pos * half;
+    const float* sn = rsin + (size_t)pos * half;
+    for (int i = tid; i < half; i += 64) {
+      float x1 = 0.f, x2 = 0.f;
+      for (int s = 0; s < splits; ++s) {
+        x1 += pr[s * split_stride + i];
+        x2 += pr[s * split_stride + i + half];
+      }
       const float o1 = x1 * cs[i] - x2 * sn[i];
       const float o2 = x2 * cs[i] + x1 * sn[i];
-      if (h < D.nh) {
-        stf(q_out, (size_t)m * D.qd + c0, o1);
-        stf(q_out, (size_t)m * D.qd + c0 + half, o2);
+      if (kslot < 0) {
+        stf(q_out, (size_t)m * D.qd + (size_t)slot * hd + i, o1);
+        stf(q_out, (size_t)m * D.qd + (size_t)slot * hd + i + half, o2);
       } else {
-        const int kvh = h - D.nh;
         for (int c = 0; c < copies; ++c) {
           const int b = tables[(size_t)(seq + c) * max_blocks + pos / D.blk];
           if (b < 0 || b >= n_blocks) { atomicOr(err, 2); continue; }
-          T* dst = kv + ((((size_t)b * D.L + layer) * D.nkv + kvh) * 2) * blk_elems + (size_t)(pos % D.blk) * hd;
+          T* dst = kv + ((((size_t)b * D.L + layer) * D.nkv + kslot) * 2) * blk_elems + (size_t)(pos % D.blk) * hd;
           stf(dst, i, o1);
           stf(dst, i + half, o2);
         }
       }
-    } else {
-      const int jv = j - nrot;  // v element
-      const int kvh = jv / hd, i = jv - kvh * hd;
-      const float v = val(D.qd + D.kvd + jv);
+    }
+  } else {
+    for (int i = tid; i < hd; i += 64) {
+      float v = 0.f;
+      for (int s = 0; s < splits; ++s) v += pr[s * split_stride + i];
       for (int c = 0; c < copies; ++c) {
         const int b = tables[(size_t)(seq + c) * max_blocks + pos / D.blk];
         if (b < 0 || b >= n_blocks) { atomicOr(err, 2); continue; }
-        T* dst = kv + ((((size_t)b * D.L + layer) * D.nkv + kvh) * 2 + 1) * blk_elems + (size_t)(pos % D.blk) * hd;
-        stf(dst, i, v);
+        T* dst = kv + ((((size_t)b * D.L + layer) * D.nkv + vslot) * 2 + 1) * blk_elems + (size_t)i * D.blk +
+                 (pos % D.blk);
+        stf(dst, 0, v);
       }
     }
   }
 }
 
-// h[m][f] = silu(g) * u, with gate/up columns interleaved in 16-column blocks
+// h[m][f] = silu(g) * u, gate and up columns interleaved in 16-column blocks
 template <typename T>
 __global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ part, int splits, int M, int ff,
                                                 T* __restrict__ h) {
   const int m = blockIdx.x;
-  const int n = 2 * ff;
-  const size_t split_stride = (size_t)M * n;
-  const float* pr = part + (size_t)m * n;
-  for (int f = threadIdx.x; f < ff; f += blockDim.x) {
-    const int cg = (f >> 4) * 32 + (f & 15);
-    float g = 0.f, u = 0.f;
-    for (int s = 0; s < splits; ++s) {
-      g += pr[s * split_stride + cg];
-      u += pr[s * split_stride + cg + 16];
+  const int g = blockIdx.y * 256 + threadIdx.x;
+  if (g >= (ff >> 3)) return;
+  const int f = g * 8;
+  const int cg = (f >> 4) * 32 + (f & 15);
+  const size_t n = 2 * (size_t)ff;
+  float gv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, uv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int s = 0; s < splits; ++s) {
+    float a[8], b[8];
+    ld8(part, ((size_t)s * M + m) * n + cg, a);
+    ld8(part, ((size_t)s * M + m) * n + cg + 16, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      gv[e] += a[e];
+      uv[e] += b[e];
     }
-    const float sg = g / (1.0f + expf(-g));
-    stf(h, (size_t)m * ff + f, sg * u);
   }
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = gv[e] / (1.0f + expf(-gv[e])) * uv[e];
+  st8(h, xoff(h, m, f, ff, (M + 15) >> 4), o);
 }
 
-// dst[p*G + g] = src[p*P + P - 1] (last prompt position, replicated over the group)
+// dst row p*G + g = src row p*P + P - 1 (last prompt position, replicated over the group), GEMM operand layout
 template <typename T>
-__global__ __launch_bounds__(256) void k_gather_rows(const T* __restrict__ src, int ld, int P, int G,
-                                                     T* __restrict__ dst) {
+__global__ __launch_bounds__(256) void k_gather_rows(const T* __restrict__ src, int d, int P, int G, int M_src,
+                                                     int M_dst, T* __restrict__ dst) {
   const int r = blockIdx.x;
-  const int p = r / G;
-  const T* s = src + ((size_t)p * P + P - 1) * ld;
-  for (int i = threadIdx.x; i < ld; i += blockDim.x) dst[(size_t)r * ld + i] = s[i];
+  const int sr = (r / G) * P + P - 1;
+  const int mb_s = (M_src + 15) >> 4, mb_d = (M_dst + 15) >> 4;
+  for (int g = threadIdx.x; g < (d >> 3); g += blockDim.x) {
+    float v[8];
+    ld8(src, xoff(src, sr, g * 8, d, mb_s), v);
+    st8(dst, xoff(dst, r, g * 8, d, mb_d), v);
+  }
 }
 
 __global__ void k_advance(int32_t* __restrict__ ctx_len, int S, int32_t* __restrict__ cols) {
@@ -200,32 +228,35 @@ hipError_t launch_qkv_epilogue(hipStream_t s, const Dims& D, const float* part, 
                                const float* rope_cos, const float* rope_sin, void* q_out, void* kv_pool, int n_blocks,
                                const int32_t* tables, int max_blocks, int layer, int32_t* err) {
   if (M <= 0) return hipSuccess;
+  const dim3 grid(M, D.nh + 2 * D.nkv);
   if (D.dtype == ROLLOUT_DTYPE_BF16)
-    hipLaunchKernelGGL(k_qkv_epilogue<uint16_t>, dim3(M), dim3(256), 0, s, D, part, splits, M, rm, rope_cos,
-                       rope_sin, (uint16_t*)q_out, (uint16_t*)kv_pool, n_blocks, tables, max_blocks, layer, err);
+    hipLaunchKernelGGL(k_qkv_epilogue<uint16_t>, grid, dim3(64), 0, s, D, part, splits, M, rm, rope_cos, rope_sin,
+                       (uint16_t*)q_out, (uint16_t*)kv_pool, n_blocks, tables, max_blocks, layer, err);
   else
-    hipLaunchKernelGGL(k_qkv_epilogue<float>, dim3(M), dim3(256), 0, s, D, part, splits, M, rm, rope_cos, rope_sin,
+    hipLaunchKernelGGL(k_qkv_epilogue<float>, grid, dim3(64), 0, s, D, part, splits, M, rm, rope_cos, rope_sin,
                        (float*)q_out, (float*)kv_pool, n_blocks, tables, max_blocks, layer, err);
   return hipGetLastError();
 }
 
 hipError_t launch_swiglu(hipStream_t s, int dtype, const float* part, int splits, int M, int ff, void* h) {
   if (M <= 0) return hipSuccess;
+  const dim3 grid(M, ((ff >> 3) + 255) / 256);
   if (dtype == ROLLOUT_DTYPE_BF16)
-    hipLaunchKernelGGL(k_swiglu<uint16_t>, dim3(M), dim3(256), 0, s, part, splits, M, ff, (uint16_t*)h);
+    hipLaunchKernelGGL(k_swiglu<uint16_t>, grid, dim3(256), 0, s, part, splits, M, ff, (uint16_t*)h);
   else
-    hipLaunchKernelGGL(k_swiglu<float>, dim3(M), dim3(256), 0, s, part, splits, M, ff, (float*)h);
+    hipLaunchKernelGGL(k_swiglu<float>, grid, dim3(256), 0, s, part, splits, M, ff, (float*)h);
   return hipGetLastError();
 }
 
-hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
+hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int d, int P, int G, int n_prompts,
                               void* dst) {
   if (n_prompts <= 0) return hipSuccess;
+  const int M_src = n_prompts * P, M_dst = n_prompts * G;
   if (dtype == ROLLOUT_DTYPE_BF16)
-    hipLaunchKernelGGL(k_gather_rows<uint16_t>, dim3(n_prompts * G), dim3(256), 0, s, (const uint16_t*)src, ld, P, G,
-                       (uint16_t*)dst);
+    hipLaunchKernelGGL(k_gather_rows<uint16_t>, dim3(M_dst), dim3(256), 0, s, (const uint16_t*)src, d, P, G, M_src,
+                       M_dst, (uint16_t*)dst);
   else
-    hipLaunchKernelGGL(k_gather_rows<float>, dim3(n_prompts * G), dim3(256), 0, s, (const float*)src, ld, P, G,
+    hipLaunchKernelGGL(k_gather_rows<float>, dim3(M_dst), dim3(256), 0, s, (const float*)src, d, P, G, M_src, M_dst,
                        (float*)dst);
   return hipGetLastError();
 }

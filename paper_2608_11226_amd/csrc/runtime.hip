@@ -151,7 +151,8 @@ Layout make_layout(const Dims& D, int S, int max_prompt_len) {
 
   Lo.S = S;
   Lo.T_chunk = prefill_chunk_rows(max_prompt_len);
-  Lo.R = std::max(S, Lo.T_chunk);
+  // activation operands are addressed in whole 16-row MFMA blocks
+  Lo.R = (std::max(S, Lo.T_chunk) + 15) / 16 * 16;
   Lo.max_blocks = (D.max_ctx + D.blk - 1) / D.blk;
   int st;
   Lo.attn_splits_max = attn_splits(D.max_ctx, &st);
@@ -162,7 +163,7 @@ Layout make_layout(const Dims& D, int S, int max_prompt_len) {
   Lo.q = take(R * D.qd * eb);
   Lo.o = take(R * D.qd * eb);
   Lo.h = take(R * D.ff * eb);
-  Lo.a_last = take((size_t)S * D.d * eb);
+  Lo.a_last = take((size_t)(S + 15) / 16 * 16 * D.d * eb);
   Lo.part = take(Lo.part_elems * 4);
   Lo.opart = take(R * D.nh * Lo.attn_splits_max * D.hd * 4);
   Lo.ml = take(R * D.nh * Lo.attn_splits_max * 2 * 4);

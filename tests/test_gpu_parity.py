@@ -222,6 +222,33 @@ def test_bf16_small_teacher_forced_logits(n_prompts, G, P):
     eng.close()
 
 
+GQA7_BF16 = (2, 256, 14, 2, 128, 512, 2048, 1e6)  # 7 query heads per KV head, head_dim 128 (the 7B ratio)
+
+
+@pytest.mark.parametrize("blk,n_prompts,G,P", [(16, 2, 8, 40), (8, 3, 2, 37), (32, 1, 4, 70), (16, 9, 1, 33)])
+def test_bf16_gqa7_teacher_forced_logits(blk, n_prompts, G, P):
+    log(f"bf16 GQA 14/2 x 128 teacher forced blk={blk} prompts={n_prompts} G={G} P={P}")
+    N = 6
+    S = n_prompts * G
+    cfg = R.model_config(GQA7_BF16, R.DTYPE_BF16, 80, N, S, kv_block_size=blk)
+    eng = R.Engine(cfg)
+    model = OracleModel(shape_of(cfg), mode="bf16")
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=41)
+    u = W.uniforms(S, N, seed=42)
+    ref = rollout(model, prompts, G, N, 1.0, 1.0, u)
+    logits = torch.empty((S, cfg.vocab), dtype=torch.float32, device="cuda:0")
+    R.rollout_prefill(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, logits)
+    eng.synchronize()
+    err = [float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][0])))]
+    for t in range(1, N):
+        R.rollout_decode_step(eng.ctx, to_dev(ref["tokens"][:, t - 1], torch), logits)
+        eng.synchronize()
+        err.append(float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][t]))))
+    log(f"  max abs logit error per step: {[round(e, 5) for e in err]}")
+    assert max(err) <= 3e-2
+    eng.close()
+
+
 def test_device_error_flag_on_bad_token():
     eng, cfg = _tiny_engine()
     prompts = W.prompts(2, 16, cfg.vocab)
