@@ -8,12 +8,14 @@
 //   X (B operand): tiles of 32 k x 16 activation rows, [K/32][M/16][64][8],
 //                  lane = m%16 + 16*((k%32)/8) -- written by the producing
 //                  kernel (norm, SwiGLU, attention combine).
-// A workgroup of four waves owns 64 weight rows (16 per wave) and a K range;
+// A workgroup of eight waves owns 128 weight rows (16 per wave) and a K range;
 // it stages X for the range through a double-buffered LDS slab shared by the
-// four waves, while the weights (read exactly once) and the next X slab are
-// already in flight in registers.  Projections with few output rows are split
-// over K so that every CU streams weights; split partials are summed in split
-// order by the consuming kernel, so results are deterministic.
+// eight waves (the X operand is re-read from L2 once per 128 weight rows, so
+// its traffic is half the weight traffic), while the weights (read exactly
+// once, non-temporally) and the next X slab are already in flight in
+// registers.  Projections with few output rows are split over K so that every
+// CU streams weights; split partials are summed in split order by the
+// consuming kernel, so results are deterministic.
 //
 // fp32 path: a plain LDS-tiled VALU GEMM over row-major X and W (the fp32
 // path exists for exact parity on small models, not for speed).
@@ -28,36 +30,50 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
-template <int MB, int KS>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
-                                                   float* __restrict__ out, int M, int N, int K, int kslice) {
-  constexpr int XV = KS * MB * 64;  // 16-byte X vectors per chunk
-  constexpr int XPT = (XV + 255) / 256;
+// MB: 16-row blocks of X per workgroup pass; KS: k-steps (of 32) per staged X slab;
+// NB: 16-row weight blocks per wave; WV: waves per workgroup; NT: non-temporal weight loads
+// (weights are read exactly once per step; keeping them out of the caches leaves room for X).
+template <int MB, int KS, int NB, int WV, bool NT>
+__global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
+                                                       float* __restrict__ out, int M, int N, int K, int kslice) {
+  constexpr int NT_ = WV * 64;
+  constexpr int XV = KS * MB * 64;  // 16-byte X vectors per slab
+  constexpr int XPT = (XV + NT_ - 1) / NT_;
   __shared__ bf16x8_t xs[2][XV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nb = blockIdx.x * 4 + wave;
-  const bool nvalid = nb * 16 < N;
+  const int nb0 = (blockIdx.x * WV + wave) * NB;  // first weight block of this wave
   const int kbt = K >> 5;
   const int Mb = (M + 15) >> 4;
   const int kb0 = (int)(blockIdx.y * kslice) >> 5;
   const int kb1 = min(kbt, kb0 + (kslice >> 5));
   const int mb0 = blockIdx.z * MB;
-  const bf16x8_t* wp = W + (size_t)(nvalid ? nb : 0) * (size_t)kbt * 64 + lane;
+  bool nvalid[NB];
+  const bf16x8_t* wp[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    nvalid[j] = (nb0 + j) * 16 < N;
+    wp[j] = W + (size_t)(nvalid[j] ? nb0 + j : 0) * (size_t)kbt * 64 + lane;
+  }
 
   bf16x8_t zero;
 #pragma unroll
   for (int e = 0; e < 8; ++e) zero[e] = (__bf16)0.0f;
-  floatx4_t acc[MB];
+  floatx4_t acc[NB][MB];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  bf16x8_t wcur[KS], wnxt[KS], xr[XPT];
-#define LOAD_W(dst, kb)                                                                \
-  _Pragma("unroll") for (int ks = 0; ks < KS; ++ks) dst[ks] =                          \
-      (nvalid && (kb) + ks < kb1) ? wp[(size_t)((kb) + ks) * 64] : zero;
+  bf16x8_t wcur[NB][KS], wnxt[NB][KS], xr[XPT];
+#define LOAD_W(dst, kb)                                                                          \
+  _Pragma("unroll") for (int j = 0; j < NB; ++j) _Pragma("unroll") for (int ks = 0; ks < KS; ++ks) \
+      dst[j][ks] = (nvalid[j] && (kb) + ks < kb1)                                                \
+                       ? (NT ? __builtin_nontemporal_load(wp[j] + (size_t)((kb) + ks) * 64)      \
+                             : wp[j][(size_t)((kb) + ks) * 64])                                   \
+                       : zero;
 #define LOAD_X(kb)                                                                      \
   _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
-    const int v = tid + 256 * j;                                                        \
+    const int v = tid + NT_ * j;                                                        \
     bf16x8_t t = zero;                                                                  \
     if (v < XV) {                                                                       \
       const int ks = v / (MB * 64), mb = (v >> 6) % MB, ln = v & 63;                    \
@@ -68,7 +84,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16x8_t* __restrict__ 
   }
 #define STORE_X(buf)                                                                    \
   _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
-    const int v = tid + 256 * j;                                                        \
+    const int v = tid + NT_ * j;                                                        \
     if (v < XV) xs[buf][v] = xr[j];                                                     \
   }
 
@@ -88,29 +104,38 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16x8_t* __restrict__ 
     for (int ks = 0; ks < KS; ++ks) {
       if (kb + ks < kb1) {
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks], xs[buf][(ks * MB + mb) * 64 + lane], acc[mb],
-                                                            0, 0, 0);
+        for (int mb = 0; mb < MB; ++mb) {
+          const bf16x8_t xf = xs[buf][(ks * MB + mb) * 64 + lane];
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[j][ks], xf, acc[j][mb], 0, 0, 0);
+        }
       }
     }
     if (more) STORE_X(buf ^ 1);
     __syncthreads();
     buf ^= 1;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) wcur[ks] = wnxt[ks];
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) wcur[j][ks] = wnxt[j][ks];
   }
 #undef LOAD_W
 #undef LOAD_X
 #undef STORE_X
-  if (!nvalid) return;
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
   float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
-  const int n = nb * 16 + 4 * (lane >> 4);
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int m = (mb0 + mb) * 16 + (lane & 15);
-    if (m < M)
-      *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]);
+  for (int j = 0; j < NB; ++j) {
+    if (!nvalid[j]) continue;
+    const int n = (nb0 + j) * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = (mb0 + mb) * 16 + (lane & 15);
+      if (m < M)
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) =
+            make_float4(acc[j][mb][0], acc[j][mb][1], acc[j][mb][2], acc[j][mb][3]);
+    }
   }
 }
 
@@ -137,6 +162,9 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   if (m < M && n < N) out[(size_t)m * N + n] = acc;
 }
 
+// weight rows per workgroup: 8 waves x 16 rows share each staged X slab
+constexpr int kRowsPerWG = 128;
+
 // m-blocks of 16 rows handled by one workgroup pass
 int mb_for(int M) {
   const int mb = (M + 15) / 16;
@@ -159,11 +187,11 @@ int kslice_for(int K, int splits) {
 
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;
-  static const int target = env_int("ROLLOUT_GEMM_TARGET_WG", 512);
-  static const int min_k = env_int("ROLLOUT_GEMM_MIN_KSLICE", 512);
+  static const int target = env_int("ROLLOUT_GEMM_TARGET_WG", 768);
+  static const int min_k = env_int("ROLLOUT_GEMM_MIN_KSLICE", 256);
   const int mb = mb_for(M);
   const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  const int nwg = (N + 63) / 64 * mchunks;
+  const int nwg = (N + kRowsPerWG - 1) / kRowsPerWG * mchunks;
   int s = (target + nwg - 1) / nwg;
   s = std::min(s, std::max(1, K / min_k));
   s = std::min(s, max_splits);
@@ -183,16 +211,16 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
   const int mb = mb_for(M);
   const int kslice = kslice_for(K, splits);
   const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  dim3 grid((N + 63) / 64, splits, mchunks);
+  dim3 grid((N + kRowsPerWG - 1) / kRowsPerWG, splits, mchunks);
   const bf16x8_t* x = (const bf16x8_t*)X;
   const bf16x8_t* w = (const bf16x8_t*)W;
   switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
-    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
-    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
-    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
-    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 4>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
-    default: hipLaunchKernelGGL((k_gemm_bf16<16, 2>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice); break;
+    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
+    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
+    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
+    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
+    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 4, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
+    default: hipLaunchKernelGGL((k_gemm_bf16<16, 2, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
   }
   return hipGetLastError();
 }

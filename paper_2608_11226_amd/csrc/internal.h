@@ -89,8 +89,11 @@ hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld,
                               void* dst);
 hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);
 hipError_t launch_set_cols(hipStream_t s, int32_t* cols, int c0, int c1);
+// Sampler scratch: stored e values of S rows plus per-chunk statistics.
+size_t sample_scratch_bytes(int S, int V);
 hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float temperature, float top_p,
-                         const float* u, int u_stride, const int32_t* col, int32_t* out, int out_stride);
+                         const float* u, int u_stride, const int32_t* col, int32_t* out, int out_stride,
+                         void* scratch);
 hipError_t launch_grpo(hipStream_t s, const float* r, int n_groups, int G, float eps, int ddof, float* adv,
                        int32_t* zero_var);
 

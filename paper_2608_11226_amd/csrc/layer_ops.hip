@@ -11,6 +11,8 @@
 // Cache block layout (blk tokens): [block][layer][kv head][K: blk x hd | V: hd x blk];
 // K is token-major, V is dimension-major so the attention kernel's P.V MFMA
 // reads four consecutive tokens of one dimension as one 8-byte load.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace rollout {
@@ -32,7 +34,7 @@ __global__ __launch_bounds__(256) void k_embed(const T* __restrict__ E, const in
 
 // x[m] += sum_s part[s][m]; out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * gain  (GEMM operand layout)
 template <typename T>
-__global__ __launch_bounds__(256) void k_residual_norm(const float* __restrict__ part, int splits, int M, int d,
+__global__ __launch_bounds__(1024) void k_residual_norm(const float* __restrict__ part, int splits, int M, int d,
                                                        float* __restrict__ x, const float* __restrict__ gain,
                                                        float eps, T* __restrict__ out) {
   __shared__ float red[32];
@@ -45,12 +47,16 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float* __restrict__
     float v[8];
     ld8(xr, (size_t)g * 8, v);
     if (part) {
+      float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll 4
       for (int s = 0; s < splits; ++s) {
         float p[8];
         ld8(part, ((size_t)s * M + m) * d + (size_t)g * 8, p);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] += p[e];
+        for (int e = 0; e < 8; ++e) acc[e] += p[e];
       }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += acc[e];
       st8(xr, (size_t)g * 8, v);
     }
 #pragma unroll
@@ -215,11 +221,13 @@ hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* 
 hipError_t launch_residual_norm(hipStream_t s, int dtype, const float* part, int splits, int M, int d, float* x,
                                 const float* gain, float eps, void* out) {
   if (M <= 0) return hipSuccess;
+  // one thread per group of 8 columns (up to 1024 threads per row)
+  const int threads = std::min(1024, ((d >> 3) + 63) / 64 * 64);
   if (dtype == ROLLOUT_DTYPE_BF16)
-    hipLaunchKernelGGL(k_residual_norm<uint16_t>, dim3(M), dim3(256), 0, s, part, splits, M, d, x, gain, eps,
+    hipLaunchKernelGGL(k_residual_norm<uint16_t>, dim3(M), dim3(threads), 0, s, part, splits, M, d, x, gain, eps,
                        (uint16_t*)out);
   else
-    hipLaunchKernelGGL(k_residual_norm<float>, dim3(M), dim3(256), 0, s, part, splits, M, d, x, gain, eps,
+    hipLaunchKernelGGL(k_residual_norm<float>, dim3(M), dim3(threads), 0, s, part, splits, M, d, x, gain, eps,
                        (float*)out);
   return hipGetLastError();
 }

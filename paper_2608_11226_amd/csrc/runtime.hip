@@ -40,7 +40,7 @@ struct Layout {
   size_t rope_cos = 0, rope_sin = 0;
   size_t weights_end = 0;  // weights + rope tables
   size_t x = 0, a = 0, q = 0, o = 0, h = 0, a_last = 0, part = 0, opart = 0, ml = 0, logits = 0;
-  size_t tables = 0, ctx_len = 0, cols = 0, err = 0;
+  size_t tables = 0, ctx_len = 0, cols = 0, err = 0, samp = 0;
   size_t work_end = 0;     // start of the KV pool
   size_t weight_bytes = 0, work_bytes = 0, kv_block_bytes = 0;
   int S = 0, R = 0, T_chunk = 0, max_blocks = 0, attn_splits_max = 1;
@@ -168,6 +168,7 @@ Layout make_layout(const Dims& D, int S, int max_prompt_len) {
   Lo.opart = take(R * D.nh * Lo.attn_splits_max * D.hd * 4);
   Lo.ml = take(R * D.nh * Lo.attn_splits_max * 2 * 4);
   Lo.logits = take((size_t)S * D.V * 4);
+  Lo.samp = take(sample_scratch_bytes(S, D.V));
   Lo.tables = take((size_t)S * Lo.max_blocks * 4 + (size_t)S * 4);  // block tables, then ctx_len
   Lo.ctx_len = Lo.tables + (size_t)S * Lo.max_blocks * 4;
   Lo.cols = take(64);
@@ -620,9 +621,13 @@ rollout_status rollout_sample(rollout_ctx* ctx, const float* d_logits, int32_t n
   if (n_seqs < 1) return fail(ctx, ROLLOUT_EINVAL, "n_seqs must be >= 1");
   if (!(temperature >= 0.f) || !std::isfinite(temperature)) return fail(ctx, ROLLOUT_EINVAL, "temperature must be >= 0");
   if (!(top_p > 0.f && top_p <= 1.f)) return fail(ctx, ROLLOUT_EINVAL, "top_p must be in (0, 1]");
-  Scope sc(ctx, 2, (double)n_seqs * ctx->D.V * 4, 0);
-  HIP_TRY(ctx, launch_sample(ctx->stream, d_logits, n_seqs, ctx->D.V, temperature, top_p, d_uniforms, 1, nullptr,
-                             d_tokens_out, 1), "sample");
+  // rows go through the sampler scratch in batches of the context's sequence capacity
+  for (int r0 = 0; r0 < n_seqs; r0 += ctx->Lo.S) {
+    const int n = std::min(ctx->Lo.S, n_seqs - r0);
+    Scope sc(ctx, 2, (double)n * ctx->D.V * 4, 0);
+    HIP_TRY(ctx, launch_sample(ctx->stream, d_logits + (size_t)r0 * ctx->D.V, n, ctx->D.V, temperature, top_p,
+                               d_uniforms + r0, 1, nullptr, d_tokens_out + r0, 1, ctx->at(ctx->Lo.samp)), "sample");
+  }
   return ROLLOUT_OK;
 }
 
@@ -671,7 +676,8 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
     if (r) return r;
     int32_t* tok = d_tokens_out + (size_t)s0 * N;
     const float* uu = d_uniforms + (size_t)s0 * N;
-    HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, nullptr, tok, N), "sample");
+    HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, nullptr, tok, N,
+                               ctx->at(ctx->Lo.samp)), "sample");
     if (N == 1) continue;
     HIP_TRY(ctx, launch_set_cols(ctx->stream, cols, 0, 1), "set cols");
     const bool use_graph = !ctx->prof.on;
@@ -679,7 +685,8 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
     auto step = [&]() -> rollout_status {
       rollout_status rr = enqueue_decode(ctx, tok, N, cols, logits, prompt_len + N);
       if (rr) return rr;
-      HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, cols + 1, tok, N), "sample");
+      HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, cols + 1, tok, N,
+                                 ctx->at(ctx->Lo.samp)), "sample");
       HIP_TRY(ctx, launch_advance(ctx->stream, nullptr, 0, cols), "advance");
       return ROLLOUT_OK;
     };
