@@ -1,25 +1,28 @@
-// Paged grouped-query attention over the KV cache, split over the context.
+// Paged grouped-query attention over the KV cache.
 //
 // Every query row attends to keys 0 .. pos of its sequence (causal), with the
-// 1/sqrt(hd) scale and a max-subtracted softmax.  The context is cut into
-// splits; each split leaves an unnormalised output with its running (max, sum)
-// and the combine kernel merges the splits with log-sum-exp weights, in split
-// order.
+// 1/sqrt(hd) scale and a max-subtracted softmax (online form: running max and
+// running sum, rescaled as new keys arrive).
 //
-// bf16 path, head_dim 64 or 128: one wavefront per (row, KV head, split).  All
-// query heads of the KV head's group ride in one MFMA (up to 16 heads): with
-// the scores computed transposed, S^T = K Q^T (16 tokens x 16 heads per
-// v_mfma_f32_16x16x32_bf16 step over hd), each lane holds the scores of one
-// head for four tokens, which is exactly the B-operand layout of the P V
-// product, so O^T = V^T P^T (v_mfma_f32_16x16x16_bf16, one per 16 output
-// dimensions) consumes the softmaxed tile straight from registers.  Softmax
-// statistics need only two cross-lane shuffles per 16-token tile.  K and V
-// tiles are read once per row and KV head, two 16-token tiles in flight per
-// wave.  P is rounded to bf16 for the MFMA (scores, softmax and accumulation
-// are fp32).
+// bf16 path, head_dim 64 or 128: one workgroup of four waves per (row, KV
+// head), covering the whole context.  All query heads of the KV head's group
+// ride in one MFMA (up to 16 heads): with the scores computed transposed,
+// S^T = K Q^T (16 tokens x 16 heads per v_mfma_f32_16x16x32_bf16 step over
+// hd), each lane holds the scores of one head for four tokens, which is
+// exactly the B-operand layout of the P V product, so O^T = V^T P^T
+// (v_mfma_f32_16x16x16_bf16, one per 16 output dimensions) consumes the
+// softmaxed tile straight from registers.  Softmax statistics need two
+// cross-lane shuffles per 16-token tile.  Wave w takes tiles w, w+4, w+8, ...
+// of the context and keeps the next tile's K/V loads in flight while it
+// computes the current one; at the end the four waves merge their (max, sum,
+// output) states through LDS and write the normalised output directly in the
+// O-projection's operand layout, so no partial results leave the workgroup.
+// K and V are read once per row and KV head.  P is rounded to bf16 for the
+// MFMA (scores, softmax and accumulation are fp32).
 //
-// fp32 path (and head_dim 32): a VALU kernel with the same split structure
-// that stages K/V tiles in LDS.
+// fp32 path (and head_dim 32): a VALU kernel split over the context that
+// stages K/V tiles in LDS; a combine kernel merges its splits with
+// log-sum-exp weights in split order.
 //
 // Cache block layout: [block][layer][kv head][K: blk x hd | V: hd x blk].
 #include "internal.h"
@@ -44,25 +47,109 @@ __device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int
 
 __device__ __forceinline__ short f2bs(float f) { return (short)f32_to_bf16(f); }
 
+// K (A operand) and V^T (A operand of P.V) fragments of one 16-token tile
+template <int HD>
+struct KVTile {
+  bf16x8_t k[HD / 32];
+  short4_t v[HD / 16];
+};
+
+template <int HD>
+__device__ __forceinline__ void load_tile(KVTile<HD>& t, int tb, int t_end, int hh, int g, const int32_t* trow,
+                                          int blk, const uint16_t* kv, size_t block_stride, size_t layer_base,
+                                          size_t blk_elems, int n_blocks, int32_t* err) {
+  bf16x8_t zero8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
+  const int tk = tb + hh;  // key row supplied by this lane
+  bool kok = false;
+  if (tk < t_end) {
+    const int b = trow[tk / blk];
+    if (b >= 0 && b < n_blocks) {
+      const uint16_t* kp = kv + (size_t)b * block_stride + layer_base + (size_t)(tk % blk) * HD + 8 * g;
+#pragma unroll
+      for (int c = 0; c < HD / 32; ++c) t.k[c] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * c);
+      kok = true;
+    } else {
+      atomicOr(err, 4);
+    }
+  }
+  if (!kok) {
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c) t.k[c] = zero8;
+  }
+  const int tv = tb + 4 * g;  // four value tokens tv .. tv+3 (never straddle a block)
+  int vmask = tv < t_end ? min(4, t_end - tv) : 0;
+  if (vmask > 0) {
+    const int b = trow[tv / blk];
+    if (b >= 0 && b < n_blocks) {
+      const uint16_t* vp = kv + (size_t)b * block_stride + layer_base + blk_elems + (tv % blk);
+#pragma unroll
+      for (int j = 0; j < HD / 16; ++j) t.v[j] = *reinterpret_cast<const short4_t*>(vp + (size_t)(16 * j + hh) * blk);
+    } else {
+      vmask = 0;
+    }
+  }
+  if (vmask < 4) {  // tokens past the context may hold stale data: never let them reach the MFMA
+#pragma unroll
+    for (int j = 0; j < HD / 16; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e >= vmask) t.v[j][e] = 0;
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void attend_tile(const KVTile<HD>& t, const bf16x8_t* qf, int tb, int t_end, int g,
+                                            float scale, float& m_run, float& l_run, floatx4_t* o) {
+  floatx4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < HD / 32; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(t.k[c], qf[c], s, 0, 0, 0);
+  // s[i] = score of token tb + 4g + i for head lane%16
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    s[i] = (tb + 4 * g + i < t_end) ? s[i] * scale : -INFINITY;
+    mx = fmaxf(mx, s[i]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(m_run, mx);
+  const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
+  float p[4], ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    p[i] = (s[i] == -INFINITY) ? 0.f : expf(s[i] - m_new);
+    ps += p[i];
+  }
+  ps += __shfl_xor(ps, 16, 64);
+  ps += __shfl_xor(ps, 32, 64);
+  l_run = l_run * alpha + ps;
+  m_run = m_new;
+  const short4_t pf = {f2bs(p[0]), f2bs(p[1]), f2bs(p[2]), f2bs(p[3])};
+#pragma unroll
+  for (int j = 0; j < HD / 16; ++j) {
+    o[j] *= alpha;
+    o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(t.v[j], pf, o[j], 0, 0, 0);
+  }
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ kv, int n_blocks,
                                                    const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
-                                                   int R, int splits, int split_tokens, int layer,
-                                                   float* __restrict__ opart, float* __restrict__ ml,
+                                                   int R, int layer, uint16_t* __restrict__ out,
                                                    int32_t* __restrict__ err) {
   constexpr int KC = HD / 32;  // QK^T k-steps
   constexpr int DT = HD / 16;  // P.V output tiles
-  const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (item >= R * D.nkv * splits) return;  // no barriers below
-  const int split = item % splits;
-  const int kvh = (item / splits) % D.nkv;
-  const int r = item / (splits * D.nkv);
+  __shared__ float s_m[4][16], s_l[4][16];
+  __shared__ float s_o[4][16][HD + 4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kvh = blockIdx.x % D.nkv;
+  const int r = blockIdx.x / D.nkv;
   int seq, pos;
   row_place(rm, r, &seq, &pos);
-  const int t_begin = split * split_tokens;
-  const int t_end = min(pos + 1, t_begin + split_tokens);
+  const int t_end = pos + 1;
   const int nrep = D.nh / D.nkv;
   const int hh = lane & 15, g = lane >> 4;
   const int blk = D.blk;
@@ -72,14 +159,12 @@ __global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __res
   const size_t block_stride = (size_t)D.L * D.nkv * kv_head_stride;
   const int32_t* trow = tables + (size_t)seq * max_blocks;
 
-  bf16x8_t zero8;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
-  const short4_t zero4 = {0, 0, 0, 0};
-
   // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
   bf16x8_t qf[KC];
   {
+    bf16x8_t zero8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
     const uint16_t* qrow = q + (size_t)r * D.qd + (size_t)(kvh * nrep + hh) * HD;
 #pragma unroll
     for (int c = 0; c < KC; ++c)
@@ -91,98 +176,53 @@ __global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __res
 #pragma unroll
   for (int j = 0; j < DT; ++j) o[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int t0 = t_begin; t0 < t_end; t0 += 32) {
-    // loads of two 16-token tiles first, so both are in flight together
-    bf16x8_t kf[2][KC];
-    short4_t vf[2][DT];
-    int vmask[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int tb = t0 + 16 * u;
-      const int tk = tb + hh;  // key row supplied by this lane
-      if (tk < t_end) {
-        const int b = trow[tk / blk];
-        if (b >= 0 && b < n_blocks) {
-          const uint16_t* kp = kv + (size_t)b * block_stride + layer_base + (size_t)(tk % blk) * HD + 8 * g;
-#pragma unroll
-          for (int c = 0; c < KC; ++c) kf[u][c] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * c);
-        } else {
-          atomicOr(err, 4);
-#pragma unroll
-          for (int c = 0; c < KC; ++c) kf[u][c] = zero8;
-        }
-      } else {
-#pragma unroll
-        for (int c = 0; c < KC; ++c) kf[u][c] = zero8;
-      }
-      const int tv = tb + 4 * g;  // four value tokens tv .. tv+3 (never straddle a block)
-      vmask[u] = tv < t_end ? min(4, t_end - tv) : 0;
-      if (vmask[u] > 0) {
-        const int b = trow[tv / blk];
-        if (b >= 0 && b < n_blocks) {
-          const uint16_t* vp = kv + (size_t)b * block_stride + layer_base + blk_elems + (tv % blk);
-#pragma unroll
-          for (int j = 0; j < DT; ++j) vf[u][j] = *reinterpret_cast<const short4_t*>(vp + (size_t)(16 * j + hh) * blk);
-        } else {
-          vmask[u] = 0;
-        }
-      }
-      if (vmask[u] < 4) {  // tokens past the context may hold stale data: never let them reach the MFMA
-#pragma unroll
-        for (int j = 0; j < DT; ++j) {
-          if (vmask[u] == 0) vf[u][j] = zero4;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (e >= vmask[u]) vf[u][j][e] = 0;
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int tb = t0 + 16 * u;
-      if (tb >= t_end) break;
-      floatx4_t s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < KC; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[c], s, 0, 0, 0);
-      // s[i] = score of token tb + 4g + i for head hh
-      float mx = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        s[i] = (tb + 4 * g + i < t_end) ? s[i] * scale : -INFINITY;
-        mx = fmaxf(mx, s[i]);
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
-      float p[4], ps = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        p[i] = (s[i] == -INFINITY) ? 0.f : expf(s[i] - m_new);
-        ps += p[i];
-      }
-      ps += __shfl_xor(ps, 16, 64);
-      ps += __shfl_xor(ps, 32, 64);
-      l_run = l_run * alpha + ps;
-      m_run = m_new;
-      const short4_t pf = {f2bs(p[0]), f2bs(p[1]), f2bs(p[2]), f2bs(p[3])};
-#pragma unroll
-      for (int j = 0; j < DT; ++j) {
-        o[j] *= alpha;
-        o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf[u][j], pf, o[j], 0, 0, 0);
-      }
-    }
+  // wave w: tiles w, w + 4, ...; two tiles in registers, the next one loading while one is computed
+  KVTile<HD> ta, tb_;
+  int t0 = 16 * wave;
+  if (t0 < t_end) load_tile<HD>(ta, t0, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
+  while (t0 < t_end) {
+    const int t1 = t0 + 64;
+    if (t1 < t_end) load_tile<HD>(tb_, t1, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
+    attend_tile<HD>(ta, qf, t0, t_end, g, scale, m_run, l_run, o);
+    if (t1 >= t_end) break;
+    const int t2 = t1 + 64;
+    if (t2 < t_end) load_tile<HD>(ta, t2, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
+    attend_tile<HD>(tb_, qf, t1, t_end, g, scale, m_run, l_run, o);
+    t0 = t2;
   }
-  // o[j][i] = unnormalised output of head hh at dimension 16 j + 4 g + i
-  if (hh < nrep) {
-    float* op = opart + (((size_t)r * D.nh + kvh * nrep + hh) * splits + split) * HD + 4 * g;
+
+  // merge the four waves: o[j][i] is head hh at dimension 16 j + 4 g + i
+  if (g == 0) {
+    s_m[wave][hh] = m_run;
+    s_l[wave][hh] = l_run;
+  }
 #pragma unroll
-    for (int j = 0; j < DT; ++j) *reinterpret_cast<float4*>(op + 16 * j) = make_float4(o[j][0], o[j][1], o[j][2], o[j][3]);
-    if (g == 0) {
-      float* mp = ml + (((size_t)r * D.nh + kvh * nrep + hh) * splits + split) * 2;
-      mp[0] = m_run;
-      mp[1] = l_run;
+  for (int j = 0; j < DT; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s_o[wave][hh][16 * j + 4 * g + i] = o[j][i];
+  __syncthreads();
+  // each thread finishes 8 consecutive dimensions of one head
+  const int Mb = (R + 15) >> 4;
+  for (int item = threadIdx.x; item < nrep * (HD / 8); item += 256) {
+    const int h = item / (HD / 8), d0 = (item % (HD / 8)) * 8;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (s_l[w][h] > 0.f) mx = fmaxf(mx, s_m[w][h]);
+    float num[8] = {0, 0, 0, 0, 0, 0, 0, 0}, den = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (s_l[w][h] > 0.f) {
+        const float wt = expf(s_m[w][h] - mx);
+        den += wt * s_l[w][h];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) num[e] += wt * s_o[w][h][d0 + e];
+      }
     }
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = den > 0.f ? num[e] / den : 0.f;
+    st8(out, xoff(out, r, (kvh * nrep + h) * HD + d0, D.qd, Mb), v);
   }
 }
 
@@ -324,10 +364,12 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ o
   st8(out, xoff(out, r, g * 8, qd, (R + 15) >> 4), o);
 }
 
+bool mfma_attention(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 && (D.hd == 128 || D.hd == 64); }
+
 }  // namespace
 
 int attn_splits(int max_ctx, int* split_tokens) {
-  const int st = 128;
+  const int st = 256;
   *split_tokens = st;
   const int s = (max_ctx + st - 1) / st;
   return s < 1 ? 1 : s;
@@ -335,17 +377,16 @@ int attn_splits(int max_ctx, int* split_tokens) {
 
 hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const void* kv_pool, int n_blocks,
                             const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
-                            int layer, float* opart, float* ml, int32_t* err) {
+                            int layer, float* opart, float* ml, void* out, int32_t* err) {
   if (R <= 0) return hipSuccess;
-  if (D.dtype == ROLLOUT_DTYPE_BF16 && (D.hd == 128 || D.hd == 64)) {
-    const int items = R * D.nkv * splits;
-    const dim3 grid((items + 3) / 4);
+  if (mfma_attention(D)) {
+    const dim3 grid((unsigned)R * D.nkv);
     if (D.hd == 128)
       hipLaunchKernelGGL(k_attn_mfma<128>, grid, dim3(256), 0, s, D, (const uint16_t*)q, (const uint16_t*)kv_pool,
-                         n_blocks, tables, max_blocks, rm, R, splits, split_tokens, layer, opart, ml, err);
+                         n_blocks, tables, max_blocks, rm, R, layer, (uint16_t*)out, err);
     else
       hipLaunchKernelGGL(k_attn_mfma<64>, grid, dim3(256), 0, s, D, (const uint16_t*)q, (const uint16_t*)kv_pool,
-                         n_blocks, tables, max_blocks, rm, R, splits, split_tokens, layer, opart, ml, err);
+                         n_blocks, tables, max_blocks, rm, R, layer, (uint16_t*)out, err);
     return hipGetLastError();
   }
   const dim3 grid((unsigned)R * D.nkv * splits);
@@ -360,18 +401,15 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const v
     else ROLLOUT_ATTN(float, 32);
   }
 #undef ROLLOUT_ATTN
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_combine(hipStream_t s, const Dims& D, const float* opart, const float* ml, int R, int splits,
-                               void* out) {
-  if (R <= 0) return hipSuccess;
-  const dim3 grid(R, ((D.qd >> 3) + 63) / 64);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // merge the context splits into the output
+  const dim3 cgrid(R, ((D.qd >> 3) + 63) / 64);
   if (D.dtype == ROLLOUT_DTYPE_BF16)
-    hipLaunchKernelGGL(k_attn_combine<uint16_t>, grid, dim3(64), 0, s, opart, ml, R, D.nh, splits, D.hd,
+    hipLaunchKernelGGL(k_attn_combine<uint16_t>, cgrid, dim3(64), 0, s, opart, ml, R, D.nh, splits, D.hd,
                        (uint16_t*)out);
   else
-    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(64), 0, s, opart, ml, R, D.nh, splits, D.hd, (float*)out);
+    hipLaunchKernelGGL(k_attn_combine<float>, cgrid, dim3(64), 0, s, opart, ml, R, D.nh, splits, D.hd, (float*)out);
   return hipGetLastError();
 }
 

@@ -79,12 +79,12 @@ hipError_t launch_qkv_epilogue(hipStream_t s, const Dims& D, const float* part, 
                                const float* rope_cos, const float* rope_sin, void* q_out, void* kv_pool,
                                int n_blocks, const int32_t* tables, int max_blocks, int layer, int32_t* err);
 hipError_t launch_swiglu(hipStream_t s, int dtype, const float* part, int splits, int M, int ff, void* h);
+// Attention of R rows over the cache, written to out in the O-projection operand
+// layout.  Paths that split the context use opart/ml (R x n_heads x splits) as scratch.
 int attn_splits(int max_ctx, int* split_tokens);
 hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const void* kv_pool, int n_blocks,
                             const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
-                            int layer, float* opart, float* ml, int32_t* err);
-hipError_t launch_attn_combine(hipStream_t s, const Dims& D, const float* opart, const float* ml, int R,
-                               int splits, void* out);
+                            int layer, float* opart, float* ml, void* out, int32_t* err);
 hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
                               void* dst);
 hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);

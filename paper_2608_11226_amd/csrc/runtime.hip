@@ -329,8 +329,7 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
       const double kvb = kv_tokens_read * D.nkv * 2.0 * D.hd * eb;
       Scope sc(c, 1, kvb + (double)M * D.qd * (eb + eb), 4.0 * kv_tokens_read * D.nh * D.hd);
       HIP_TRY(c, launch_attention(c->stream, D, q, kv, c->n_blocks, tables, Lo.max_blocks, rm, M, asplits, st_tok, l,
-                                  opart, ml, err), "attention");
-      HIP_TRY(c, launch_attn_combine(c->stream, D, opart, ml, M, asplits, o), "attention combine");
+                                  opart, ml, o, err), "attention");
     }
     r = gemm(c, o, c->at(y.wo), part, M, D.d, D.qd, kMaxSplits, &s);
     if (r) return r;
