@@ -12,17 +12,18 @@
 // Masses are fixed-point integers, floor(e * 2^40) (exact for e >= 2^-16,
 // under 2^-40 of error each otherwise), so every sum, scan and comparison is
 // exact integer arithmetic and the draw does not depend on scheduling.  The
-// top-p threshold is a most-significant-digit radix select over the IEEE bit
-// patterns of e (monotonic for e >= 0): four 8-bit digits with mass
-// histograms.
+// top-p threshold tau is a most-significant-digit radix select over the IEEE
+// bit patterns of e (monotonic for e >= 0): four 8-bit digits, each digit
+// chosen from mass histograms.  Ties at tau are kept lowest id first.
 //
-// Three launches per batch of rows: (1) per-chunk maxima of y, (2) e_i
-// computed once and stored, with per-chunk masses and first-digit histograms
-// (rows x chunks workgroups keep every CU busy), (3) one workgroup per row
-// finishes the radix select and the ordered draw reading only the stored e.
-// Every pass over a row is coalesced: for the ordered draw each wave owns a
-// contiguous segment of ids, segment totals are scanned across waves, and only
-// the wave whose segment holds the crossing walks it, 64 ids at a time.
+// Every pass over a row's V values runs as rows x chunks workgroups (chunk
+// max; exp stored once with the chunk mass and first-digit histogram; one
+// histogram pass per remaining digit; per-chunk kept mass and tie count);
+// between passes a small kernel per row picks the digit with a parallel
+// suffix scan over the 256 bins.  The final kernel per row scans the chunk
+// totals, finds the chunk holding the crossing, and walks only that chunk:
+// one contiguous segment per wave, segment totals scanned across waves, then
+// the crossing wave scans its segment 64 ids at a time.
 #include "internal.h"
 
 #include <climits>
@@ -30,10 +31,23 @@
 namespace rollout {
 namespace {
 
-constexpr int SB = 1024;  // threads of the per-row kernels
-constexpr int NW = SB / 64;
-constexpr int CB = 256;   // threads of the per-chunk kernels
+constexpr int CB = 256;  // threads of the per-chunk kernels
+constexpr int CW = CB / 64;
+constexpr int RB = 1024;  // threads of the per-row draw kernel
+constexpr int RW = RB / 64;
 typedef unsigned long long u64;
+
+// per-row selection state shared by the passes
+struct RowSel {
+  u64 total;   // mass of the row
+  u64 target;  // ceil(top_p * total): mass the kept set must reach
+  u64 above;   // mass of values strictly above the selected prefix
+  unsigned prefix, mask;
+  u64 kties;   // ties at tau that are kept (lowest ids first)
+  u64 kept;    // kept mass
+  float m;     // max of y
+  int pad;
+};
 
 // floor(e * 2^40) for 0 <= e <= 1, by shifting the significand
 __device__ __forceinline__ u64 fx40(float e) {
@@ -61,38 +75,53 @@ __device__ __forceinline__ u64 wave_incl_scan(u64 v, int lane) {
   return v;
 }
 
-__global__ __launch_bounds__(SB) void k_argmax(const float* __restrict__ logits, int V,
-                                               const int32_t* __restrict__ col, int32_t* __restrict__ out,
-                                               int out_stride) {
-  __shared__ float redf[NW];
-  __shared__ int redi[NW];
-  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+// ---------------------------------------------------------------------------
+// greedy
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void better(float& best, int& bi, float v, int i) {
+  if (v > best || (v == best && i < bi)) { best = v; bi = i; }
+}
+
+__global__ __launch_bounds__(CB) void k_chunk_argmax(const float* __restrict__ logits, int V, int chunk,
+                                                     float* __restrict__ cval, int* __restrict__ cidx) {
+  __shared__ float rv[CW];
+  __shared__ int ri[CW];
+  const int row = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const float* z = logits + (size_t)row * V;
+  const int lo = c * chunk, hi = min(V, lo + chunk);
   float best = -INFINITY;
   int bi = INT_MAX;
-  for (int i = tid; i < V; i += SB) {
-    const float v = z[i];
-    if (v > best) { best = v; bi = i; }
-  }
+  for (int i = lo + tid; i < hi; i += CB) better(best, bi, z[i], i);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(best, o, 64);
-    const int oi = __shfl_xor(bi, o, 64);
-    if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
-  }
-  if (lane == 0) { redf[w] = best; redi[w] = bi; }
+  for (int o = 32; o > 0; o >>= 1) better(best, bi, __shfl_xor(best, o, 64), __shfl_xor(bi, o, 64));
+  if (lane == 0) { rv[w] = best; ri[w] = bi; }
   __syncthreads();
   if (tid == 0) {
-    for (int i = 1; i < NW; ++i)
-      if (redf[i] > best || (redf[i] == best && redi[i] < bi)) { best = redf[i]; bi = redi[i]; }
-    out[(size_t)row * out_stride + (col ? col[0] : 0)] = bi == INT_MAX ? 0 : bi;
+    for (int j = 1; j < CW; ++j) better(best, bi, rv[j], ri[j]);
+    cval[(size_t)row * gridDim.y + c] = best;
+    cidx[(size_t)row * gridDim.y + c] = bi;
   }
 }
 
-// (1) cmax[row][c] = max over chunk c of fp32(z / T)
+__global__ __launch_bounds__(64) void k_argmax_final(const float* __restrict__ cval, const int* __restrict__ cidx,
+                                                     int nc, const int32_t* __restrict__ col, int32_t* __restrict__ out,
+                                                     int out_stride) {
+  const int row = blockIdx.x, lane = threadIdx.x;
+  float best = -INFINITY;
+  int bi = INT_MAX;
+  for (int c = lane; c < nc; c += 64) better(best, bi, cval[(size_t)row * nc + c], cidx[(size_t)row * nc + c]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) better(best, bi, __shfl_xor(best, o, 64), __shfl_xor(bi, o, 64));
+  if (lane == 0) out[(size_t)row * out_stride + (col ? col[0] : 0)] = bi == INT_MAX ? 0 : bi;
+}
+
+// ---------------------------------------------------------------------------
+// sampling
+// ---------------------------------------------------------------------------
+// cmax[row][c] = max over chunk c of fp32(z / T)
 __global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logits, int V, int chunk, float T,
                                                   float* __restrict__ cmax) {
-  __shared__ float red[CB / 64];
+  __shared__ float red[CW];
   const int row = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
   const float* z = logits + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
@@ -102,17 +131,17 @@ __global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logi
   if ((tid & 63) == 0) red[tid >> 6] = mx;
   __syncthreads();
   if (tid == 0) {
-    for (int j = 1; j < CB / 64; ++j) mx = fmaxf(mx, red[j]);
+    for (int j = 1; j < CW; ++j) mx = fmaxf(mx, red[j]);
     cmax[(size_t)row * gridDim.y + c] = mx;
   }
 }
 
-// (2) e = exp(y - m) stored; per-chunk mass; first-digit mass histogram when filtering
+// e = exp(y - m) stored; chunk mass; first-digit (bits 24..31) mass histogram when filtering
 __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logits, int V, int chunk, float T,
                                                   const float* __restrict__ cmax, float* __restrict__ escr,
                                                   u64* __restrict__ cmass, u64* __restrict__ chist, int filter) {
-  __shared__ u64 hist[CB / 64][256];
-  __shared__ u64 red[CB / 64];
+  __shared__ u64 hist[CW][256];
+  __shared__ u64 red[CW];
   const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
   float m = -INFINITY;
   for (int j = 0; j < nc; ++j) m = fmaxf(m, cmax[(size_t)row * nc + j]);
@@ -120,7 +149,7 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
   float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
   if (filter) {
-    for (int i = tid; i < (CB / 64) * 256; i += CB) (&hist[0][0])[i] = 0;
+    for (int i = tid; i < CW * 256; i += CB) (&hist[0][0])[i] = 0;
     __syncthreads();
   }
   u64 mass = 0;
@@ -136,115 +165,184 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
   __syncthreads();
   if (tid == 0) {
     u64 t = 0;
-    for (int j = 0; j < CB / 64; ++j) t += red[j];
+    for (int j = 0; j < CW; ++j) t += red[j];
     cmass[(size_t)row * nc + c] = t;
   }
   if (filter) {
     u64 t = 0;
-    for (int j = 0; j < CB / 64; ++j) t += hist[j][tid];
+    for (int j = 0; j < CW; ++j) t += hist[j][tid];
     chist[((size_t)row * nc + c) * 256 + tid] = t;
   }
 }
 
-// (3) finish the radix select and draw, one workgroup per row
-__global__ __launch_bounds__(SB) void k_select_draw(const float* __restrict__ escr, int V, int nc, float top_p,
-                                                    const u64* __restrict__ cmass, const u64* __restrict__ chist,
-                                                    const float* __restrict__ u, int u_stride,
-                                                    const int32_t* __restrict__ col, int32_t* __restrict__ out,
-                                                    int out_stride) {
-  __shared__ u64 hist[NW][256];
-  __shared__ u64 redu[NW], redt[NW];
-  __shared__ u64 sh_above;
-  __shared__ unsigned sh_prefix;
-  __shared__ int sh_tok;
+// Pick the digit at `shift`: the largest d with above + sum_{j >= d} hist[j] >= target.
+// One workgroup of 256 threads per row; thread t owns digit 255 - t for the suffix scan.
+__global__ __launch_bounds__(256) void k_select_digit(const u64* __restrict__ chist, const u64* __restrict__ cmass,
+                                                      int nc, float top_p, int shift, RowSel* __restrict__ sel) {
+  __shared__ u64 wtot[4];
+  __shared__ int wcnt[4];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const float* e_row = escr + (size_t)row * V;
-  const int c = col ? col[0] : 0;
-
-  u64 total = 0;
-  for (int j = 0; j < nc; ++j) total += cmass[(size_t)row * nc + j];
-
-  const bool filter = top_p < 1.0f;
-  unsigned tau = 0;
-  u64 ftau = 0, kties = 0, kept = total;
-  if (filter) {
+  RowSel st = sel[row];
+  if (shift == 24) {  // first digit: initialise the row state from the chunk masses
+    u64 total = 0;
+    for (int j = 0; j < nc; ++j) total += cmass[(size_t)row * nc + j];
+    st.total = total;
     u64 target = (u64)ceil((double)top_p * (double)total);
-    if (target > total) target = total;
-    if (target == 0) target = 1;
-    unsigned prefix = 0, mask = 0;
-    u64 above = 0;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      if (shift == 24) {
-        if (tid < 256) {
-          u64 t = 0;
-          for (int j = 0; j < nc; ++j) t += chist[((size_t)row * nc + j) * 256 + tid];
-          hist[0][tid] = t;
-        }
-        __syncthreads();
-      } else {
-        for (int i = tid; i < NW * 256; i += SB) (&hist[0][0])[i] = 0;
-        __syncthreads();
-        for (int i = tid; i < V; i += SB) {
-          const float e = e_row[i];
-          const unsigned b = __float_as_uint(e);
-          if ((b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(e));
-        }
-        __syncthreads();
-        if (tid < 256) {
-          u64 t = 0;
-          for (int j = 0; j < NW; ++j) t += hist[j][tid];
-          hist[0][tid] = t;
-        }
-        __syncthreads();
-      }
-      if (tid == 0) {
-        u64 cum = above;
-        int sel = 0;
-        for (int dgt = 255; dgt >= 0; --dgt) {
-          if (cum + hist[0][dgt] >= target) { sel = dgt; break; }
-          cum += hist[0][dgt];
-        }
-        sh_above = cum;
-        sh_prefix = prefix | ((unsigned)sel << shift);
-      }
-      __syncthreads();
-      above = sh_above;
-      prefix = sh_prefix;
-      mask |= 255u << shift;
-      __syncthreads();
-    }
-    tau = prefix;
-    ftau = fx40(__uint_as_float(tau));
-    const u64 need = target - above;
-    kties = ftau ? (need + ftau - 1) / ftau : (u64)V;
-    kept = above + kties * ftau;
+    st.target = target > total ? total : (target == 0 ? 1 : target);
+    st.above = 0;
+    st.prefix = 0;
+    st.mask = 0;
   }
+  const int d = 255 - tid;
+  u64 h = 0;
+  for (int j = 0; j < nc; ++j) h += chist[((size_t)row * nc + j) * 256 + d];
+  // inclusive scan in thread order = suffix sum over digits >= d
+  u64 inc = wave_incl_scan(h, lane);
+  if (lane == 63) wtot[w] = inc;
+  __syncthreads();
+  for (int j = 0; j < w; ++j) inc += wtot[j];
+  const bool reach = st.above + inc >= st.target;  // true exactly for digits 0 .. d*
+  const unsigned long long bal = __ballot(reach);
+  if (lane == 0) wcnt[w] = __popcll(bal);
+  __syncthreads();
+  // reach holds for threads tid >= 255 - d*, i.e. the count of true lanes is d* + 1
+  const int dsel = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3] - 1;
+  if (d == dsel) {
+    st.above = st.above + inc - h;  // mass of digits above dsel
+    st.prefix |= (unsigned)dsel << shift;
+    st.mask |= 255u << shift;
+    if (shift == 0) {
+      const u64 ftau = fx40(__uint_as_float(st.prefix));
+      const u64 need = st.target - st.above;
+      st.kties = ftau ? (need + ftau - 1) / ftau : 0;
+      st.kept = st.above + st.kties * ftau;
+    }
+    sel[row] = st;
+  }
+}
 
-  // ordered draw: wave w owns ids [w*seg, w*seg + seg)
-  const int seg = ((V + NW - 1) / NW + 63) / 64 * 64;
-  const int lo = min(V, w * seg), hi = min(V, lo + seg);
-  u64 gt_mass = 0, ties = 0;
-  for (int i = lo + lane; i < hi; i += 64) {
+// mass histogram of the digit at `shift` over values matching the selected prefix
+__global__ __launch_bounds__(CB) void k_chunk_hist(const float* __restrict__ escr, int V, int chunk, int shift,
+                                                   const RowSel* __restrict__ sel, u64* __restrict__ chist) {
+  __shared__ u64 hist[CW][256];
+  const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
+  const unsigned prefix = sel[row].prefix, mask = sel[row].mask;
+  const float* e_row = escr + (size_t)row * V;
+  const int lo = c * chunk, hi = min(V, lo + chunk);
+  for (int i = tid; i < CW * 256; i += CB) (&hist[0][0])[i] = 0;
+  __syncthreads();
+  for (int i = lo + tid; i < hi; i += CB) {
     const float e = e_row[i];
     const unsigned b = __float_as_uint(e);
-    if (!filter || b > tau) gt_mass += fx40(e);
+    if ((b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(e));
+  }
+  __syncthreads();
+  u64 t = 0;
+  for (int j = 0; j < CW; ++j) t += hist[j][tid];
+  chist[((size_t)row * nc + c) * 256 + tid] = t;
+}
+
+// per chunk: mass of kept values strictly above tau (all values without filtering) and ties at tau
+__global__ __launch_bounds__(CB) void k_chunk_kept(const float* __restrict__ escr, int V, int chunk, int filter,
+                                                   const RowSel* __restrict__ sel, u64* __restrict__ cgt,
+                                                   u64* __restrict__ cties) {
+  __shared__ u64 r1[CW], r2[CW];
+  const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
+  const unsigned tau = filter ? sel[row].prefix : 0u;
+  const float* e_row = escr + (size_t)row * V;
+  const int lo = c * chunk, hi = min(V, lo + chunk);
+  u64 gt = 0, ties = 0;
+  for (int i = lo + tid; i < hi; i += CB) {
+    const float e = e_row[i];
+    const unsigned b = __float_as_uint(e);
+    if (!filter || b > tau) gt += fx40(e);
     else if (b == tau) ties += 1;
   }
-  gt_mass = wave_sum_u64(gt_mass);
+  gt = wave_sum_u64(gt);
   ties = wave_sum_u64(ties);
-  if (lane == 0) redt[w] = ties;
-  if (tid == 0) sh_tok = -1;
+  if ((tid & 63) == 0) { r1[w] = gt; r2[w] = ties; }
   __syncthreads();
-  u64 ties_before = 0;
-  for (int j = 0; j < w; ++j) ties_before += redt[j];
+  if (tid == 0) {
+    u64 a = 0, b = 0;
+    for (int j = 0; j < CW; ++j) { a += r1[j]; b += r2[j]; }
+    cgt[(size_t)row * nc + c] = a;
+    cties[(size_t)row * nc + c] = b;
+  }
+}
+
+// the ordered draw: locate the crossing chunk from chunk totals, then walk that chunk only
+__global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int V, int chunk, int nc, int filter,
+                                             const RowSel* __restrict__ sel, const u64* __restrict__ cgt,
+                                             const u64* __restrict__ cties, const u64* __restrict__ cmass,
+                                             const float* __restrict__ u, int u_stride,
+                                             const int32_t* __restrict__ col, int32_t* __restrict__ out,
+                                             int out_stride) {
+  __shared__ u64 s_mass[RW], s_ties[RW];
+  __shared__ int s_chunk, s_tok;
+  __shared__ u64 s_excl, s_ties_before, s_thresh;
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c_out = col ? col[0] : 0;
+  const float* e_row = escr + (size_t)row * V;
+  unsigned tau = 0;
+  u64 ftau = 0, kties = 0, kept = 0;
+  if (filter) {
+    const RowSel st = sel[row];
+    tau = st.prefix;
+    ftau = fx40(__uint_as_float(tau));
+    kties = st.kties;
+    kept = st.kept;
+  } else {
+    for (int j = 0; j < nc; ++j) kept += cmass[(size_t)row * nc + j];
+  }
+  if (w == 0) {
+    // chunk scan in one wave (nc <= 64): kept mass per chunk = gt + its kept ties
+    const u64 gt = lane < nc ? cgt[(size_t)row * nc + lane] : 0;
+    const u64 ti = lane < nc ? cties[(size_t)row * nc + lane] : 0;
+    const u64 ties_incl = wave_incl_scan(ti, lane);
+    const u64 ties_before = ties_incl - ti;
+    const u64 kt = filter ? (kties > ties_before ? min(kties - ties_before, ti) : 0) : 0;
+    const u64 km = gt + kt * ftau;
+    const u64 incl = wave_incl_scan(km, lane);
+    // thresh < kept always (u < 1 and kept >= 2^40), so some chunk holds the crossing
+    const u64 thresh = (u64)((double)u[(size_t)row * u_stride + c_out] * (double)kept);
+    const unsigned long long hit = __ballot(lane < nc && km > 0 && incl > thresh);
+    const int first = hit ? __ffsll((long long)hit) - 1 : max(0, nc - 1);
+    if (lane == first) {
+      s_chunk = lane;
+      s_excl = incl - km;
+      s_ties_before = ties_before;
+      s_thresh = thresh;
+    }
+    if (lane == 0) s_tok = -1;
+  }
+  __syncthreads();
+  const int c = s_chunk;
+  const u64 thresh = s_thresh;
+  // segments of the crossing chunk, one per wave
+  const int lo_c = c * chunk, hi_c = min(V, lo_c + chunk);
+  const int seg = ((hi_c - lo_c + RW - 1) / RW + 63) / 64 * 64;
+  const int lo = min(hi_c, lo_c + w * seg), hi = min(hi_c, lo + seg);
+  u64 gt = 0, ties = 0;
+  for (int i = lo + lane; i < hi; i += 64) {
+    const unsigned b = __float_as_uint(e_row[i]);
+    if (!filter || b > tau) gt += fx40(e_row[i]);
+    else if (b == tau) ties += 1;
+  }
+  gt = wave_sum_u64(gt);
+  ties = wave_sum_u64(ties);
+  if (lane == 0) { s_mass[w] = gt; s_ties[w] = ties; }
+  __syncthreads();
+  u64 ties_before = s_ties_before, excl = s_excl;
+  for (int j = 0; j < w; ++j) ties_before += s_ties[j];
   const u64 my_kept_ties = filter ? (kties > ties_before ? min(kties - ties_before, ties) : 0) : 0;
-  const u64 my_mass = gt_mass + my_kept_ties * ftau;
-  if (lane == 0) redu[w] = my_mass;
-  __syncthreads();
-  u64 excl = 0;
-  for (int j = 0; j < w; ++j) excl += redu[j];
-  // thresh < kept always (u < 1 and kept >= 2^40), so some kept id crosses it
-  const u64 thresh = (u64)((double)u[(size_t)row * u_stride + c] * (double)kept);
+  // kept mass before this wave's segment within the chunk
+  for (int j = 0; j < w; ++j) {
+    u64 tb = s_ties_before;
+    for (int i = 0; i < j; ++i) tb += s_ties[i];
+    const u64 ktj = filter ? (kties > tb ? min(kties - tb, s_ties[j]) : 0) : 0;
+    excl += s_mass[j] + ktj * ftau;
+  }
+  const u64 my_mass = gt + my_kept_ties * ftau;
   if (my_mass > 0 && excl <= thresh && thresh < excl + my_mass) {
     u64 carry = excl, tie_carry = 0;
     for (int base = lo; base < hi; base += 64) {
@@ -261,14 +359,14 @@ __global__ __launch_bounds__(SB) void k_select_draw(const float* __restrict__ es
       const u64 cum = carry + wave_incl_scan(keep ? fx40(e) : 0ull, lane);
       const unsigned long long hit = __ballot(keep && cum > thresh);
       if (hit) {
-        if (lane == __ffsll((long long)hit) - 1) sh_tok = i;
+        if (lane == __ffsll((long long)hit) - 1) s_tok = i;
         break;
       }
       carry = __shfl(cum, 63, 64);
     }
   }
   __syncthreads();
-  if (tid == 0) out[(size_t)row * out_stride + c] = sh_tok < 0 ? 0 : sh_tok;
+  if (tid == 0) out[(size_t)row * out_stride + c_out] = s_tok < 0 ? 0 : s_tok;
 }
 
 }  // namespace
@@ -280,33 +378,48 @@ int sample_chunks(int V) {
 
 size_t sample_scratch_bytes(int S, int V) {
   const int nc = sample_chunks(V);
-  return (size_t)S * V * 4 + (size_t)S * nc * (4 + 8 + 256 * 8) + 1024;
+  return (size_t)S * V * 4 + (size_t)S * nc * (4 + 4 + 8 * 4 + 256 * 8) + (size_t)S * sizeof(RowSel) + 4096;
 }
 
 hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float temperature, float top_p,
                          const float* u, int u_stride, const int32_t* col, int32_t* out, int out_stride,
                          void* scratch) {
   if (S <= 0) return hipSuccess;
-  if (temperature == 0.0f) {
-    hipLaunchKernelGGL(k_argmax, dim3(S), dim3(SB), 0, s, logits, V, col, out, out_stride);
-    return hipGetLastError();
-  }
   const int nc = sample_chunks(V);
   const int chunk = (V + nc - 1) / nc;
   char* p = (char*)scratch;
-  float* escr = (float*)p;
-  p += ((size_t)S * V * 4 + 255) / 256 * 256;
-  u64* cmass = (u64*)p;
-  p += ((size_t)S * nc * 8 + 255) / 256 * 256;
-  float* cmax = (float*)p;
-  p += ((size_t)S * nc * 4 + 255) / 256 * 256;
-  u64* chist = (u64*)p;
+  auto take = [&](size_t bytes) {
+    char* q = p;
+    p += (bytes + 255) / 256 * 256;
+    return q;
+  };
+  float* escr = (float*)take((size_t)S * V * 4);
+  float* cmax = (float*)take((size_t)S * nc * 4);
+  int* cidx = (int*)take((size_t)S * nc * 4);
+  u64* cmass = (u64*)take((size_t)S * nc * 8);
+  u64* cgt = (u64*)take((size_t)S * nc * 8);
+  u64* cties = (u64*)take((size_t)S * nc * 8);
+  u64* chist = (u64*)take((size_t)S * nc * 256 * 8);
+  RowSel* sel = (RowSel*)take((size_t)S * sizeof(RowSel));
+  const dim3 rc(S, nc);
+  if (temperature == 0.0f) {
+    hipLaunchKernelGGL(k_chunk_argmax, rc, dim3(CB), 0, s, logits, V, chunk, cmax, cidx);
+    hipLaunchKernelGGL(k_argmax_final, dim3(S), dim3(64), 0, s, cmax, cidx, nc, col, out, out_stride);
+    return hipGetLastError();
+  }
   const int filter = top_p < 1.0f;
-  hipLaunchKernelGGL(k_chunk_max, dim3(S, nc), dim3(CB), 0, s, logits, V, chunk, temperature, cmax);
-  hipLaunchKernelGGL(k_chunk_exp, dim3(S, nc), dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass,
-                     chist, filter);
-  hipLaunchKernelGGL(k_select_draw, dim3(S), dim3(SB), 0, s, escr, V, nc, top_p, cmass, chist, u, u_stride, col,
-                     out, out_stride);
+  hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax);
+  hipLaunchKernelGGL(k_chunk_exp, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass, chist,
+                     filter);
+  if (filter) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (shift != 24) hipLaunchKernelGGL(k_chunk_hist, rc, dim3(CB), 0, s, escr, V, chunk, shift, sel, chist);
+      hipLaunchKernelGGL(k_select_digit, dim3(S), dim3(256), 0, s, chist, cmass, nc, top_p, shift, sel);
+    }
+  }
+  hipLaunchKernelGGL(k_chunk_kept, rc, dim3(CB), 0, s, escr, V, chunk, filter, sel, cgt, cties);
+  hipLaunchKernelGGL(k_draw, dim3(S), dim3(RB), 0, s, escr, V, chunk, nc, filter, sel, cgt, cties, cmass, u,
+                     u_stride, col, out, out_stride);
   return hipGetLastError();
 }
 
