@@ -4,7 +4,7 @@
 // 1/sqrt(hd) scale and a max-subtracted softmax (online form: running max and
 // running sum, rescaled as new keys arrive).
 //
-// bf16 path, head_dim 64 or 128: one workgroup of four waves per (row, KV
+// bf16 path, head_dim 64 or 128: one workgroup of NW waves per (row, KV
 // head), covering the whole context.  All query heads of the KV head's group
 // ride in one MFMA (up to 16 heads): with the scores computed transposed,
 // S^T = K Q^T (16 tokens x 16 heads per v_mfma_f32_16x16x32_bf16 step over
@@ -12,9 +12,9 @@
 // exactly the B-operand layout of the P V product, so O^T = V^T P^T
 // (v_mfma_f32_16x16x16_bf16, one per 16 output dimensions) consumes the
 // softmaxed tile straight from registers.  Softmax statistics need two
-// cross-lane shuffles per 16-token tile.  Wave w takes tiles w, w+4, w+8, ...
+// cross-lane shuffles per 16-token tile.  Wave w takes tiles w, w+NW, ...
 // of the context and keeps the next tile's K/V loads in flight while it
-// computes the current one; at the end the four waves merge their (max, sum,
+// computes the current one; at the end the waves merge their (max, sum,
 // output) states through LDS and write the normalised output directly in the
 // O-projection's operand layout, so no partial results leave the workgroup.
 // K and V are read once per row and KV head.  P is rounded to bf16 for the
@@ -25,6 +25,8 @@
 // log-sum-exp weights in split order.
 //
 // Cache block layout: [block][layer][kv head][K: blk x hd | V: hd x blk].
+#include <cstdlib>
+
 #include "internal.h"
 
 namespace rollout {
@@ -134,22 +136,37 @@ __device__ __forceinline__ void attend_tile(const KVTile<HD>& t, const bf16x8_t*
   }
 }
 
-template <int HD>
-__global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
-                                                   const uint16_t* __restrict__ kv, int n_blocks,
-                                                   const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
-                                                   int R, int layer, uint16_t* __restrict__ out,
-                                                   int32_t* __restrict__ err) {
+// Decode rows may form their own q, k, v from the QKV projection's split-K
+// partials (part[split][row][nqkv], summed in split order): rotary embedding
+// on q and k, bf16 rounding, k and v appended to the cache.  The current token
+// then enters the softmax as one more state beside the waves' states, so no
+// wave reads the cache entry this workgroup is writing.
+struct AttnQKV {
+  const float* part;  // NULL: q is read from the q buffer and the cache already holds the current token
+  int splits;
+  const float* rope_cos;
+  const float* rope_sin;
+};
+
+template <int HD, int NW, bool FQ>
+__global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
+                                                       uint16_t* __restrict__ kv, int n_blocks,
+                                                       const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
+                                                       int R, int layer, AttnQKV Q, uint16_t* __restrict__ out,
+                                                       int32_t* __restrict__ err) {
   constexpr int KC = HD / 32;  // QK^T k-steps
   constexpr int DT = HD / 16;  // P.V output tiles
-  __shared__ float s_m[4][16], s_l[4][16];
-  __shared__ float s_o[4][16][HD + 4];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int NT = NW * 64;
+  __shared__ float s_m[NW][16], s_l[NW][16];
+  __shared__ float s_o[NW][16][HD + 4];
+  __shared__ __align__(16) uint16_t s_q[FQ ? 16 : 1][HD];
+  __shared__ float s_kv[FQ ? 2 : 1][HD];  // current token's k (rotated) and v, bf16 values
+  __shared__ float s_cur[16];             // current token's scaled score per head
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kvh = blockIdx.x % D.nkv;
   const int r = blockIdx.x / D.nkv;
   int seq, pos;
   row_place(rm, r, &seq, &pos);
-  const int t_end = pos + 1;
   const int nrep = D.nh / D.nkv;
   const int hh = lane & 15, g = lane >> 4;
   const int blk = D.blk;
@@ -158,40 +175,97 @@ __global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __res
   const size_t layer_base = ((size_t)layer * D.nkv + kvh) * kv_head_stride;
   const size_t block_stride = (size_t)D.L * D.nkv * kv_head_stride;
   const int32_t* trow = tables + (size_t)seq * max_blocks;
+  const float scale = 1.0f / sqrtf((float)HD);
+  bf16x8_t zero8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
 
   // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
   bf16x8_t qf[KC];
-  {
-    bf16x8_t zero8;
+  int t_end = pos + 1;  // keys read from the cache
+  if constexpr (FQ) {
+    t_end = pos;
+    constexpr int half = HD / 2;
+    const size_t n = D.nqkv, ss = (size_t)R * n;
+    const float* pr = Q.part + (size_t)r * n;
+    const float* cs = Q.rope_cos + (size_t)pos * half;
+    const float* sn = Q.rope_sin + (size_t)pos * half;
+    const int b = trow[pos / blk];
+    const bool bok = b >= 0 && b < n_blocks;
+    uint16_t* kdst = kv + (size_t)(bok ? b : 0) * block_stride + layer_base;
+    const int npair = (nrep + 1) * half;
+    for (int it = tid; it < npair + HD; it += NT) {
+      if (it < npair) {
+        const int h = it / half, i = it - h * half;
+        const int c = (h < nrep ? (kvh * nrep + h) * HD : D.qd + kvh * HD) + i;
+        float x1 = 0.f, x2 = 0.f;
+        for (int sp = 0; sp < Q.splits; ++sp) {
+          x1 += pr[sp * ss + c];
+          x2 += pr[sp * ss + c + half];
+        }
+        const uint16_t b1 = f32_to_bf16(x1 * cs[i] - x2 * sn[i]);
+        const uint16_t b2 = f32_to_bf16(x2 * cs[i] + x1 * sn[i]);
+        if (h < nrep) {
+          s_q[h][i] = b1;
+          s_q[h][i + half] = b2;
+        } else {
+          s_kv[0][i] = bf16_to_f32(b1);
+          s_kv[0][i + half] = bf16_to_f32(b2);
+          if (bok) {
+            kdst[(size_t)(pos % blk) * HD + i] = b1;
+            kdst[(size_t)(pos % blk) * HD + i + half] = b2;
+          }
+        }
+      } else {
+        const int i = it - npair;
+        const int c = D.qd + D.kvd + kvh * HD + i;
+        float v = 0.f;
+        for (int sp = 0; sp < Q.splits; ++sp) v += pr[sp * ss + c];
+        const uint16_t bv = f32_to_bf16(v);
+        s_kv[1][i] = bf16_to_f32(bv);
+        if (bok) kdst[blk_elems + (size_t)i * blk + pos % blk] = bv;
+      }
+    }
+    if (!bok && tid == 0) atomicOr(err, 2);
+    for (int it = tid; it < (16 - nrep) * HD; it += NT) s_q[nrep + it / HD][it % HD] = 0;
+    __syncthreads();
 #pragma unroll
-    for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
+    for (int c = 0; c < KC; ++c) qf[c] = *reinterpret_cast<const bf16x8_t*>(&s_q[hh][32 * c + 8 * g]);
+    // score of the current token: one wave per head
+    for (int h = wave; h < nrep; h += NW) {
+      float acc = 0.f;
+      for (int d = lane; d < HD; d += 64) acc += bf16_to_f32(s_q[h][d]) * s_kv[0][d];
+      acc = wave_sum(acc);
+      if (lane == 0) s_cur[h] = acc * scale;
+    }
+  } else {
     const uint16_t* qrow = q + (size_t)r * D.qd + (size_t)(kvh * nrep + hh) * HD;
 #pragma unroll
     for (int c = 0; c < KC; ++c)
       qf[c] = hh < nrep ? *reinterpret_cast<const bf16x8_t*>(qrow + 32 * c + 8 * g) : zero8;
   }
-  const float scale = 1.0f / sqrtf((float)HD);
   float m_run = -INFINITY, l_run = 0.f;
   floatx4_t o[DT];
 #pragma unroll
   for (int j = 0; j < DT; ++j) o[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  // wave w: tiles w, w + 4, ...; two tiles in registers, the next one loading while one is computed
+  // wave w: tiles w, w + NW, ...; two tiles in registers, the next one loading while one is computed
+  constexpr int STRIDE = 16 * NW;
   KVTile<HD> ta, tb_;
   int t0 = 16 * wave;
   if (t0 < t_end) load_tile<HD>(ta, t0, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
   while (t0 < t_end) {
-    const int t1 = t0 + 64;
+    const int t1 = t0 + STRIDE;
     if (t1 < t_end) load_tile<HD>(tb_, t1, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
     attend_tile<HD>(ta, qf, t0, t_end, g, scale, m_run, l_run, o);
     if (t1 >= t_end) break;
-    const int t2 = t1 + 64;
+    const int t2 = t1 + STRIDE;
     if (t2 < t_end) load_tile<HD>(ta, t2, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
     attend_tile<HD>(tb_, qf, t1, t_end, g, scale, m_run, l_run, o);
     t0 = t2;
   }
 
-  // merge the four waves: o[j][i] is head hh at dimension 16 j + 4 g + i
+  // merge the waves: o[j][i] is head hh at dimension 16 j + 4 g + i
   if (g == 0) {
     s_m[wave][hh] = m_run;
     s_l[wave][hh] = l_run;
@@ -203,21 +277,27 @@ __global__ __launch_bounds__(256) void k_attn_mfma(Dims D, const uint16_t* __res
   __syncthreads();
   // each thread finishes 8 consecutive dimensions of one head
   const int Mb = (R + 15) >> 4;
-  for (int item = threadIdx.x; item < nrep * (HD / 8); item += 256) {
+  for (int item = tid; item < nrep * (HD / 8); item += NT) {
     const int h = item / (HD / 8), d0 = (item % (HD / 8)) * 8;
-    float mx = -INFINITY;
+    float mx = FQ ? s_cur[h] : -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+    for (int w = 0; w < NW; ++w)
       if (s_l[w][h] > 0.f) mx = fmaxf(mx, s_m[w][h]);
     float num[8] = {0, 0, 0, 0, 0, 0, 0, 0}, den = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       if (s_l[w][h] > 0.f) {
         const float wt = expf(s_m[w][h] - mx);
         den += wt * s_l[w][h];
 #pragma unroll
         for (int e = 0; e < 8; ++e) num[e] += wt * s_o[w][h][d0 + e];
       }
+    }
+    if constexpr (FQ) {
+      const float wt = expf(s_cur[h] - mx);
+      den += wt;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) num[e] += wt * s_kv[1][d0 + e];
     }
     float v[8];
 #pragma unroll
@@ -375,18 +455,42 @@ int attn_splits(int max_ctx, int* split_tokens) {
   return s < 1 ? 1 : s;
 }
 
-hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const void* kv_pool, int n_blocks,
+bool attention_forms_qkv(const Dims& D) { return mfma_attention(D); }
+
+hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* kv_pool, int n_blocks,
                             const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
-                            int layer, float* opart, float* ml, void* out, int32_t* err) {
+                            int layer, float* opart, float* ml, void* out, int32_t* err, const float* qkv_part,
+                            int qkv_splits, const float* rope_cos, const float* rope_sin) {
   if (R <= 0) return hipSuccess;
+  if (qkv_part && (!mfma_attention(D) || rm.P != 0)) return hipErrorInvalidValue;
   if (mfma_attention(D)) {
+    static const int nw = [] {
+      const char* v = std::getenv("ROLLOUT_ATTN_WAVES");
+      const int w = v ? std::atoi(v) : 8;
+      return w == 4 ? 4 : 8;
+    }();
     const dim3 grid((unsigned)R * D.nkv);
-    if (D.hd == 128)
-      hipLaunchKernelGGL(k_attn_mfma<128>, grid, dim3(256), 0, s, D, (const uint16_t*)q, (const uint16_t*)kv_pool,
-                         n_blocks, tables, max_blocks, rm, R, layer, (uint16_t*)out, err);
-    else
-      hipLaunchKernelGGL(k_attn_mfma<64>, grid, dim3(256), 0, s, D, (const uint16_t*)q, (const uint16_t*)kv_pool,
-                         n_blocks, tables, max_blocks, rm, R, layer, (uint16_t*)out, err);
+    const AttnQKV Q{qkv_part, qkv_splits, rope_cos, rope_sin};
+    const uint16_t* qq = (const uint16_t*)q;
+    uint16_t* kk = (uint16_t*)kv_pool;
+    uint16_t* oo = (uint16_t*)out;
+#define ROLLOUT_MFMA_ATTN(HD, NW, FQ)                                                                              \
+  hipLaunchKernelGGL((k_attn_mfma<HD, NW, FQ>), grid, dim3(NW * 64), 0, s, D, qq, kk, n_blocks, tables, max_blocks, rm, \
+                     R, layer, Q, oo, err)
+#define ROLLOUT_MFMA_ATTN_NW(HD, FQ)         \
+  do {                                       \
+    if (nw == 4) ROLLOUT_MFMA_ATTN(HD, 4, FQ); \
+    else ROLLOUT_MFMA_ATTN(HD, 8, FQ);       \
+  } while (0)
+    if (D.hd == 128) {
+      if (qkv_part) ROLLOUT_MFMA_ATTN_NW(128, true);
+      else ROLLOUT_MFMA_ATTN_NW(128, false);
+    } else {
+      if (qkv_part) ROLLOUT_MFMA_ATTN_NW(64, true);
+      else ROLLOUT_MFMA_ATTN_NW(64, false);
+    }
+#undef ROLLOUT_MFMA_ATTN_NW
+#undef ROLLOUT_MFMA_ATTN
     return hipGetLastError();
   }
   const dim3 grid((unsigned)R * D.nkv * splits);

@@ -1,21 +1,26 @@
-// Projection GEMMs: out[split][m][n] = sum_{k in split} X[m][k] * W[n][k], fp32 result.
+// Projection GEMMs: y[m][n] = sum_k X[m][k] * W[n][k], fp32 accumulation.
 //
 // bf16 path (CDNA4 MFMA, v_mfma_f32_16x16x32_bf16).  Both operands live in
 // HBM in MFMA operand order, so every global load is a fully coalesced
-// 16-byte-per-lane read and every LDS access is conflict-free:
+// 16-byte-per-lane read:
 //   W (A operand): tiles of 16 weight rows x 32 k, [N/16][K/32][64 lanes][8],
 //                  lane = row%16 + 16*((k%32)/8) -- written once at synthesis;
 //   X (B operand): tiles of 32 k x 16 activation rows, [K/32][M/16][64][8],
 //                  lane = m%16 + 16*((k%32)/8) -- written by the producing
-//                  kernel (norm, SwiGLU, attention combine).
-// A workgroup of eight waves owns 128 weight rows (16 per wave) and a K range;
-// it stages X for the range through a double-buffered LDS slab shared by the
-// eight waves (the X operand is re-read from L2 once per 128 weight rows, so
-// its traffic is half the weight traffic), while the weights (read exactly
-// once, non-temporally) and the next X slab are already in flight in
-// registers.  Projections with few output rows are split over K so that every
-// CU streams weights; split partials are summed in split order by the
-// consuming kernel, so results are deterministic.
+//                  kernel (norm, SwiGLU, attention).
+// Weights are read exactly once per step, with non-temporal loads (keeping
+// them out of the caches leaves room for the activations).
+//
+// k_gemm_bf16 (many output columns: gate/up, LM head, and every prefill
+// projection): a workgroup of eight waves owns 128 weight rows (16 per wave)
+// and a K range; it stages X through a double-buffered LDS slab shared by the
+// eight waves (X is re-read from L2 once per 128 weight rows), while the
+// weights and the next slab are in flight in registers.  With several K
+// splits each writes a partial [split][M][N] that the consumer sums in split
+// order.  The SwiGLU variant (decode gate/up, one split) finishes in
+// registers: gate row i and up row i are adjacent weight rows, so the lane
+// that holds one also holds the other, and h goes straight to the down
+// projection's operand layout.
 //
 // fp32 path: a plain LDS-tiled VALU GEMM over row-major X and W (the fp32
 // path exists for exact parity on small models, not for speed).
@@ -30,50 +35,44 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
 // MB: 16-row blocks of X per workgroup pass; KS: k-steps (of 32) per staged X slab;
-// NB: 16-row weight blocks per wave; WV: waves per workgroup; NT: non-temporal weight loads
-// (weights are read exactly once per step; keeping them out of the caches leaves room for X).
-template <int MB, int KS, int NB, int WV, bool NT>
+// WV: waves per workgroup (16 weight rows each); SWI: finish with SwiGLU (one split).
+template <int MB, int KS, int WV, bool SWI>
 __global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
-                                                       float* __restrict__ out, int M, int N, int K, int kslice) {
-  constexpr int NT_ = WV * 64;
+                                                       float* __restrict__ out, int M, int N, int K, int kslice,
+                                                       uint16_t* __restrict__ h) {
+  constexpr int NTH = WV * 64;
   constexpr int XV = KS * MB * 64;  // 16-byte X vectors per slab
-  constexpr int XPT = (XV + NT_ - 1) / NT_;
+  constexpr int XPT = (XV + NTH - 1) / NTH;
   __shared__ bf16x8_t xs[2][XV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nb0 = (blockIdx.x * WV + wave) * NB;  // first weight block of this wave
+  const int nb = blockIdx.x * WV + wave;  // this wave's 16-row weight block
+  const bool nvalid = nb * 16 < N;
   const int kbt = K >> 5;
   const int Mb = (M + 15) >> 4;
   const int kb0 = (int)(blockIdx.y * kslice) >> 5;
   const int kb1 = min(kbt, kb0 + (kslice >> 5));
   const int mb0 = blockIdx.z * MB;
-  bool nvalid[NB];
-  const bf16x8_t* wp[NB];
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    nvalid[j] = (nb0 + j) * 16 < N;
-    wp[j] = W + (size_t)(nvalid[j] ? nb0 + j : 0) * (size_t)kbt * 64 + lane;
-  }
+  const bf16x8_t* wp = W + (size_t)(nvalid ? nb : 0) * (size_t)kbt * 64 + lane;
 
   bf16x8_t zero;
 #pragma unroll
   for (int e = 0; e < 8; ++e) zero[e] = (__bf16)0.0f;
-  floatx4_t acc[NB][MB];
+  floatx4_t acc[MB];
 #pragma unroll
-  for (int j = 0; j < NB; ++j)
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  bf16x8_t wcur[NB][KS], wnxt[NB][KS], xr[XPT];
-#define LOAD_W(dst, kb)                                                                          \
-  _Pragma("unroll") for (int j = 0; j < NB; ++j) _Pragma("unroll") for (int ks = 0; ks < KS; ++ks) \
-      dst[j][ks] = (nvalid[j] && (kb) + ks < kb1)                                                \
-                       ? (NT ? __builtin_nontemporal_load(wp[j] + (size_t)((kb) + ks) * 64)      \
-                             : wp[j][(size_t)((kb) + ks) * 64])                                   \
-                       : zero;
+  bf16x8_t wcur[KS], wnxt[KS], xr[XPT];
+#define LOAD_W(dst, kb)                                               \
+  _Pragma("unroll") for (int ks = 0; ks < KS; ++ks) dst[ks] =         \
+      (nvalid && (kb) + ks < kb1) ? __builtin_nontemporal_load(wp + (size_t)((kb) + ks) * 64) : zero;
 #define LOAD_X(kb)                                                                      \
   _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
-    const int v = tid + NT_ * j;                                                        \
+    const int v = tid + NTH * j;                                                        \
     bf16x8_t t = zero;                                                                  \
     if (v < XV) {                                                                       \
       const int ks = v / (MB * 64), mb = (v >> 6) % MB, ln = v & 63;                    \
@@ -84,7 +83,7 @@ __global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restric
   }
 #define STORE_X(buf)                                                                    \
   _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
-    const int v = tid + NT_ * j;                                                        \
+    const int v = tid + NTH * j;                                                        \
     if (v < XV) xs[buf][v] = xr[j];                                                     \
   }
 
@@ -104,37 +103,42 @@ __global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restric
     for (int ks = 0; ks < KS; ++ks) {
       if (kb + ks < kb1) {
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          const bf16x8_t xf = xs[buf][(ks * MB + mb) * 64 + lane];
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[j][ks], xf, acc[j][mb], 0, 0, 0);
-        }
+        for (int mb = 0; mb < MB; ++mb)
+          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks], xs[buf][(ks * MB + mb) * 64 + lane], acc[mb],
+                                                            0, 0, 0);
       }
     }
     if (more) STORE_X(buf ^ 1);
     __syncthreads();
     buf ^= 1;
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) wcur[j][ks] = wnxt[j][ks];
+    for (int ks = 0; ks < KS; ++ks) wcur[ks] = wnxt[ks];
   }
 #undef LOAD_W
 #undef LOAD_X
 #undef STORE_X
+  if (!nvalid) return;
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
-  float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
+  const int n = nb * 16 + 4 * (lane >> 4);
+  if constexpr (SWI) {
+    // rows n, n+1 are (gate, up) of output f = n/2; rows n+2, n+3 of output f + 1
+    const int ff = N >> 1, f = n >> 1;
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    if (!nvalid[j]) continue;
-    const int n = (nb0 + j) * 16 + 4 * (lane >> 4);
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = (mb0 + mb) * 16 + (lane & 15);
+      if (m < M) {
+        const float g0 = acc[mb][0], u0 = acc[mb][1], g1 = acc[mb][2], u1 = acc[mb][3];
+        const float h0 = g0 / (1.0f + expf(-g0)) * u0, h1 = g1 / (1.0f + expf(-g1)) * u1;
+        *reinterpret_cast<uint32_t*>(h + xoff(h, m, f, ff, Mb)) = pack_bf16x2(h0, h1);
+      }
+    }
+  } else {
+    float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const int m = (mb0 + mb) * 16 + (lane & 15);
       if (m < M)
-        *reinterpret_cast<float4*>(o + (size_t)m * N + n) =
-            make_float4(acc[j][mb][0], acc[j][mb][1], acc[j][mb][2], acc[j][mb][3]);
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]);
     }
   }
 }
@@ -162,9 +166,6 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   if (m < M && n < N) out[(size_t)m * N + n] = acc;
 }
 
-// weight rows per workgroup: 8 waves x 16 rows share each staged X slab
-constexpr int kRowsPerWG = 128;
-
 // m-blocks of 16 rows handled by one workgroup pass
 int mb_for(int M) {
   const int mb = (M + 15) / 16;
@@ -183,6 +184,33 @@ int kslice_for(int K, int splits) {
   return (per + 31) / 32 * 32;
 }
 
+template <int WV, bool SWI>
+hipError_t launch_bf16(hipStream_t s, const void* X, const void* W, float* out, int M, int N, int K, int splits,
+                       uint16_t* h) {
+  const int mb = mb_for(M);
+  const int kslice = kslice_for(K, splits);
+  const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
+  const dim3 grid((N + WV * 16 - 1) / (WV * 16), splits, mchunks);
+  const dim3 block(WV * 64);
+  const bf16x8_t* x = (const bf16x8_t*)X;
+  const bf16x8_t* w = (const bf16x8_t*)W;
+  switch (mb) {
+    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 8:
+      if constexpr (SWI) return hipErrorInvalidValue;
+      else hipLaunchKernelGGL((k_gemm_bf16<8, 4, WV, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+      break;
+    default:
+      if constexpr (SWI) return hipErrorInvalidValue;
+      else hipLaunchKernelGGL((k_gemm_bf16<16, 2, WV, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+      break;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
@@ -191,7 +219,7 @@ int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   static const int min_k = env_int("ROLLOUT_GEMM_MIN_KSLICE", 256);
   const int mb = mb_for(M);
   const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  const int nwg = (N + kRowsPerWG - 1) / kRowsPerWG * mchunks;
+  const int nwg = (N + kGemmTileRows - 1) / kGemmTileRows * mchunks;
   int s = (target + nwg - 1) / nwg;
   s = std::min(s, std::max(1, K / min_k));
   s = std::min(s, max_splits);
@@ -208,21 +236,16 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
     hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, s, (const float*)X, ldx, (const float*)W, out, M, N, K);
     return hipGetLastError();
   }
-  const int mb = mb_for(M);
-  const int kslice = kslice_for(K, splits);
-  const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  dim3 grid((N + kRowsPerWG - 1) / kRowsPerWG, splits, mchunks);
-  const bf16x8_t* x = (const bf16x8_t*)X;
-  const bf16x8_t* w = (const bf16x8_t*)W;
-  switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
-    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
-    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
-    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
-    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 4, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
-    default: hipLaunchKernelGGL((k_gemm_bf16<16, 2, 1, 8, true>), grid, dim3(512), 0, s, x, w, out, M, N, K, kslice); break;
-  }
-  return hipGetLastError();
+  return launch_bf16<kGemmTileRows / 16, false>(s, X, W, out, M, N, K, splits, nullptr);
+}
+
+hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h) {
+  if (M <= 0) return hipSuccess;
+  if (M > kSwigluMaxRows || N % 4) return hipErrorInvalidValue;
+  static const int wv = env_int("ROLLOUT_SWIGLU_WAVES", 4);
+  // 64-row workgroups: twice as many as 128-row ones, which balances the CUs better
+  if (wv == 8) return launch_bf16<8, true>(s, X, W, nullptr, M, N, K, 1, (uint16_t*)h);
+  return launch_bf16<4, true>(s, X, W, nullptr, M, N, K, 1, (uint16_t*)h);
 }
 
 }  // namespace rollout

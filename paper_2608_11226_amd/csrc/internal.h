@@ -35,7 +35,7 @@ enum WLayout : int {
 enum WFuse : int {
   FUSE_NONE = 0,  // one tensor: id0, row = physical row
   FUSE_QKV = 1,   // rows [0,a) id0, [a,a+b) id1, [a+b,a+2b) id2
-  FUSE_GU = 2,    // 16-row blocks alternate id0 (gate) and id1 (up)
+  FUSE_GU = 2,    // rows alternate id0 (gate row i at 2i) and id1 (up row i at 2i + 1)
 };
 
 struct WeightDesc {
@@ -70,6 +70,13 @@ int gemm_splits(int dtype, int M, int N, int K, int max_splits);
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const void* W, float* out, int M,
                        int N, int K, int splits);
 
+constexpr int kGemmTileRows = 128;  // weight rows (output columns) per workgroup of the split-K kernel
+// Decode gate/up projection with SwiGLU applied to its own output (bf16, one
+// K split, M <= kSwigluMaxRows): W holds gate row i at physical row 2i and up
+// row i at 2i + 1; h[m][i] = silu(gate) * up in the down projection's operand layout.
+constexpr int kSwigluMaxRows = 64;
+hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h);
+
 hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
                         const int32_t* col, int M, int d, int V, float* x, int32_t* err);
 // x[m] += sum_s part[s][m] (part may be NULL); out[m] = rmsnorm(x[m]) * gain in the cache dtype.
@@ -81,10 +88,15 @@ hipError_t launch_qkv_epilogue(hipStream_t s, const Dims& D, const float* part, 
 hipError_t launch_swiglu(hipStream_t s, int dtype, const float* part, int splits, int M, int ff, void* h);
 // Attention of R rows over the cache, written to out in the O-projection operand
 // layout.  Paths that split the context use opart/ml (R x n_heads x splits) as scratch.
+// With qkv_part (decode rows, attention_forms_qkv(D) only) the kernel forms q,
+// k and v from the QKV projection's split partials itself (rotary embedding,
+// cache append) instead of reading q and expecting the cache to hold the row's token.
 int attn_splits(int max_ctx, int* split_tokens);
-hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, const void* kv_pool, int n_blocks,
+bool attention_forms_qkv(const Dims& D);
+hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* kv_pool, int n_blocks,
                             const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
-                            int layer, float* opart, float* ml, void* out, int32_t* err);
+                            int layer, float* opart, float* ml, void* out, int32_t* err, const float* qkv_part,
+                            int qkv_splits, const float* rope_cos, const float* rope_sin);
 hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
                               void* dst);
 hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);

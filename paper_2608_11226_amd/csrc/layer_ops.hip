@@ -147,7 +147,7 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue(Dims D, const float* __rest
   }
 }
 
-// h[m][f] = silu(g) * u, gate and up columns interleaved in 16-column blocks
+// h[m][f] = silu(g) * u, gate column f at 2f and up column f at 2f + 1
 template <typename T>
 __global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ part, int splits, int M, int ff,
                                                 T* __restrict__ h) {
@@ -155,22 +155,21 @@ __global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ part, 
   const int g = blockIdx.y * 256 + threadIdx.x;
   if (g >= (ff >> 3)) return;
   const int f = g * 8;
-  const int cg = (f >> 4) * 32 + (f & 15);
   const size_t n = 2 * (size_t)ff;
-  float gv[8] = {0, 0, 0, 0, 0, 0, 0, 0}, uv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float gu[16] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
   for (int s = 0; s < splits; ++s) {
     float a[8], b[8];
-    ld8(part, ((size_t)s * M + m) * n + cg, a);
-    ld8(part, ((size_t)s * M + m) * n + cg + 16, b);
+    ld8(part, ((size_t)s * M + m) * n + 2 * f, a);
+    ld8(part, ((size_t)s * M + m) * n + 2 * f + 8, b);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      gv[e] += a[e];
-      uv[e] += b[e];
+      gu[e] += a[e];
+      gu[8 + e] += b[e];
     }
   }
   float o[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = gv[e] / (1.0f + expf(-gv[e])) * uv[e];
+  for (int e = 0; e < 8; ++e) o[e] = gu[2 * e] / (1.0f + expf(-gu[2 * e])) * gu[2 * e + 1];
   st8(h, xoff(h, m, f, ff, (M + 15) >> 4), o);
 }
 

@@ -291,6 +291,14 @@ rollout_status gemm(rollout_ctx* c, const void* X, const void* W, float* out, in
   return ROLLOUT_OK;
 }
 
+// Decode gate/up GEMM with SwiGLU applied to its own output (bf16, M <= kSwigluMaxRows).
+rollout_status gemm_swiglu(rollout_ctx* c, const void* X, const void* W, int M, int N, int K, void* h) {
+  const double eb = (double)elem_bytes(c->D.dtype);
+  Scope sc(c, 0, (double)N * K * eb + (double)M * K * eb + (double)M * (N / 2) * eb, 2.0 * M * N * K);
+  HIP_TRY(c, launch_gemm_swiglu(c->stream, X, W, M, N, K, h), "gemm");
+  return ROLLOUT_OK;
+}
+
 // One transformer pass over M rows (prefill chunk or decode batch). On return
 // c->Lo.a holds the final-normed hidden states (cache dtype).
 rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max, double kv_tokens_read) {
@@ -320,7 +328,9 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
     int s;
     rollout_status r = gemm(c, a, c->at(y.wqkv), part, M, D.nqkv, D.d, kMaxSplits, &s);
     if (r) return r;
-    {
+    // decode rows: attention rotates q/k and appends k/v itself, straight from the split partials
+    const bool attn_qkv = rm.P == 0 && attention_forms_qkv(D);
+    if (!attn_qkv) {
       Scope sc(c, 2, (double)s * M * D.nqkv * 4 + (double)M * (D.qd + 2 * D.kvd) * eb, 0);
       HIP_TRY(c, launch_qkv_epilogue(c->stream, D, part, s, M, rm, c->at<float>(Lo.rope_cos), c->at<float>(Lo.rope_sin),
                                      q, kv, c->n_blocks, tables, Lo.max_blocks, l, err), "qkv epilogue");
@@ -329,7 +339,8 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
       const double kvb = kv_tokens_read * D.nkv * 2.0 * D.hd * eb;
       Scope sc(c, 1, kvb + (double)M * D.qd * (eb + eb), 4.0 * kv_tokens_read * D.nh * D.hd);
       HIP_TRY(c, launch_attention(c->stream, D, q, kv, c->n_blocks, tables, Lo.max_blocks, rm, M, asplits, st_tok, l,
-                                  opart, ml, o, err), "attention");
+                                  opart, ml, o, err, attn_qkv ? part : nullptr, s, c->at<float>(Lo.rope_cos),
+                                  c->at<float>(Lo.rope_sin)), "attention");
     }
     r = gemm(c, o, c->at(y.wo), part, M, D.d, D.qd, kMaxSplits, &s);
     if (r) return r;
@@ -338,9 +349,10 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
       HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, part, s, M, D.d, x, c->at<float>(y.mlp_norm), D.eps, a),
               "residual norm");
     }
-    r = gemm(c, a, c->at(y.wgu), part, M, 2 * D.ff, D.d, kMaxSplits, &s);
-    if (r) return r;
-    {
+    if (D.dtype == ROLLOUT_DTYPE_BF16 && M <= kSwigluMaxRows) {
+      if ((r = gemm_swiglu(c, a, c->at(y.wgu), M, 2 * D.ff, D.d, h))) return r;
+    } else {
+      if ((r = gemm(c, a, c->at(y.wgu), part, M, 2 * D.ff, D.d, kMaxSplits, &s))) return r;
       Scope sc(c, 2, (double)s * M * 2 * D.ff * 4 + (double)M * D.ff * eb, 0);
       HIP_TRY(c, launch_swiglu(c->stream, D.dtype, part, s, M, D.ff, h), "swiglu");
     }

@@ -59,9 +59,8 @@ __device__ __forceinline__ void row_source(const WeightDesc& w, int prow, int* w
     else if (prow < w.a + w.b) { *which = 1; *lrow = prow - w.a; }
     else { *which = 2; *lrow = prow - w.a - w.b; }
   } else if (w.fuse == FUSE_GU) {
-    const int pair = prow >> 5, r = prow & 31;
-    *which = r < 16 ? 0 : 1;
-    *lrow = pair * 16 + (r & 15);
+    *which = prow & 1;
+    *lrow = prow >> 1;
   } else {
     *which = 0;
     *lrow = prow;
@@ -95,7 +94,7 @@ __global__ void k_export(const T* __restrict__ src, WeightDesc w, int which, int
     const int r = (int)(i / (size_t)w.cols), c = (int)(i % (size_t)w.cols);
     int prow = r;
     if (w.fuse == FUSE_QKV) prow = which == 0 ? r : (which == 1 ? w.a + r : w.a + w.b + r);
-    else if (w.fuse == FUSE_GU) prow = (r >> 4) * 32 + (which ? 16 : 0) + (r & 15);
+    else if (w.fuse == FUSE_GU) prow = 2 * r + which;
     size_t p;
     if (w.layout == W_TILED) {
       const int nb = prow >> 4, kb = c >> 5;
