@@ -11,16 +11,24 @@
 // Weights are read exactly once per step, with non-temporal loads (keeping
 // them out of the caches leaves room for the activations).
 //
-// k_gemm_bf16 (many output columns: gate/up, LM head, and every prefill
-// projection): a workgroup of eight waves owns 128 weight rows (16 per wave)
-// and a K range; it stages X through a double-buffered LDS slab shared by the
-// eight waves (X is re-read from L2 once per 128 weight rows), while the
-// weights and the next slab are in flight in registers.  With several K
-// splits each writes a partial [split][M][N] that the consumer sums in split
-// order.  The SwiGLU variant (decode gate/up, one split) finishes in
+// k_gemm_ring (decode, M <= 64 rows): one wave per workgroup owns NBW
+// 16-row weight blocks and one K split.  Weight and activation fragments
+// stream through a D-deep register ring with no LDS and no barriers; every
+// load is unconditional (addresses clamped into range, surplus steps masked at
+// the MFMA), so the compiler keeps D - 1 ring stages in flight instead of
+// draining the load queue at every step.  X is read from L2 by every wave,
+// which costs M/(16 NBW) of the weight bytes in L2 traffic and nothing in HBM.
+// With several K splits each writes a partial [split][M][N] that the consumer
+// sums in split order.  The SwiGLU variant (gate/up, one split) finishes in
 // registers: gate row i and up row i are adjacent weight rows, so the lane
 // that holds one also holds the other, and h goes straight to the down
 // projection's operand layout.
+//
+// k_gemm_bf16 (prefill and other batches above 64 rows): a workgroup of
+// eight waves owns 128 weight rows (16 per wave) and a K range; it stages X
+// through a double-buffered LDS slab shared by the eight waves (X is re-read
+// from L2 once per 128 weight rows), while the weights and the next slab are
+// in flight in registers; split partials as above.
 //
 // fp32 path: a plain LDS-tiled VALU GEMM over row-major X and W (the fp32
 // path exists for exact parity on small models, not for speed).
@@ -40,11 +48,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // MB: 16-row blocks of X per workgroup pass; KS: k-steps (of 32) per staged X slab;
-// WV: waves per workgroup (16 weight rows each); SWI: finish with SwiGLU (one split).
-template <int MB, int KS, int WV, bool SWI>
+// WV: waves per workgroup (16 weight rows each).
+template <int MB, int KS, int WV>
 __global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
-                                                       float* __restrict__ out, int M, int N, int K, int kslice,
-                                                       uint16_t* __restrict__ h) {
+                                                       float* __restrict__ out, int M, int N, int K, int kslice) {
   constexpr int NTH = WV * 64;
   constexpr int XV = KS * MB * 64;  // 16-byte X vectors per slab
   constexpr int XPT = (XV + NTH - 1) / NTH;
@@ -120,25 +127,94 @@ __global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restric
   if (!nvalid) return;
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
   const int n = nb * 16 + 4 * (lane >> 4);
-  if constexpr (SWI) {
-    // rows n, n+1 are (gate, up) of output f = n/2; rows n+2, n+3 of output f + 1
-    const int ff = N >> 1, f = n >> 1;
+  float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int m = (mb0 + mb) * 16 + (lane & 15);
-      if (m < M) {
-        const float g0 = acc[mb][0], u0 = acc[mb][1], g1 = acc[mb][2], u1 = acc[mb][3];
-        const float h0 = g0 / (1.0f + expf(-g0)) * u0, h1 = g1 / (1.0f + expf(-g1)) * u1;
-        *reinterpret_cast<uint32_t*>(h + xoff(h, m, f, ff, Mb)) = pack_bf16x2(h0, h1);
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = (mb0 + mb) * 16 + (lane & 15);
+    if (m < M)
+      *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]);
+  }
+}
+
+// MB = ceil(M/16) row blocks of X; NBW weight blocks per wave; D ring stages.
+template <int MB, int NBW, int D, bool SWI>
+__global__ __launch_bounds__(64) void k_gemm_ring(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
+                                                  float* __restrict__ out, int M, int N, int K, int kslice,
+                                                  uint16_t* __restrict__ h) {
+  const int lane = threadIdx.x;
+  const int nb0 = blockIdx.x * NBW;
+  const int nbt = N >> 4, kbt = K >> 5;
+  const int kb0 = (int)blockIdx.y * (kslice >> 5);
+  const int nk = min(kbt, kb0 + (kslice >> 5)) - kb0;
+  if (nk <= 0) {  // an empty K split contributes zeros
+    if constexpr (!SWI) {
+      for (int j = 0; j < NBW && nb0 + j < nbt; ++j)
+        for (int m = lane & 15; m < M; m += 16)
+          *reinterpret_cast<float4*>(out + ((size_t)blockIdx.y * M + m) * N + (nb0 + j) * 16 + 4 * (lane >> 4)) =
+              make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    return;
+  }
+  floatx4_t acc[NBW][MB];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  {
+    const bf16x8_t* wp[NBW];
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) wp[j] = W + ((size_t)min(nb0 + j, nbt - 1) * kbt + kb0) * 64 + lane;
+    const bf16x8_t* xp = XF + (size_t)kb0 * MB * 64 + lane;
+    bf16x8_t wr[D][NBW], xr[D][MB];
+    // ring stage d holds k-step min(i, nk - 1); steps past nk reload the last one and are not used
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const size_t kk = (size_t)min(d, nk - 1);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) xr[d][mb] = xp[(kk * MB + mb) * 64];
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) wr[d][j] = __builtin_nontemporal_load(wp[j] + kk * 64);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int i = 0; i < nk; i += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        if (i + d < nk) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int j = 0; j < NBW; ++j)
+              acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wr[d][j], xr[d][mb], acc[j][mb], 0, 0, 0);
+        }
+        const size_t kk = (size_t)min(i + d + D, nk - 1);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) xr[d][mb] = xp[(kk * MB + mb) * 64];
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) wr[d][j] = __builtin_nontemporal_load(wp[j] + kk * 64);
+        // keeps the ring order through scheduling, so each stage waits only for its own loads
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-  } else {
-    float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
+  }
+  // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    if (nb0 + j >= nbt) continue;
+    const int n = (nb0 + j) * 16 + 4 * (lane >> 4);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-      const int m = (mb0 + mb) * 16 + (lane & 15);
-      if (m < M)
-        *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]);
+      const int m = mb * 16 + (lane & 15);
+      if (m >= M) continue;
+      if constexpr (SWI) {
+        // rows n, n+1 are (gate, up) of output f = n/2; rows n+2, n+3 of output f + 1
+        const float g0 = acc[j][mb][0], u0 = acc[j][mb][1], g1 = acc[j][mb][2], u1 = acc[j][mb][3];
+        const float h0 = g0 / (1.0f + expf(-g0)) * u0, h1 = g1 / (1.0f + expf(-g1)) * u1;
+        *reinterpret_cast<uint32_t*>(h + xoff(h, m, n >> 1, N >> 1, MB)) = pack_bf16x2(h0, h1);
+      } else {
+        float* o = out + (size_t)blockIdx.y * M * N;
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) =
+            make_float4(acc[j][mb][0], acc[j][mb][1], acc[j][mb][2], acc[j][mb][3]);
+      }
     }
   }
 }
@@ -184,29 +260,48 @@ int kslice_for(int K, int splits) {
   return (per + 31) / 32 * 32;
 }
 
-template <int WV, bool SWI>
-hipError_t launch_bf16(hipStream_t s, const void* X, const void* W, float* out, int M, int N, int K, int splits,
-                       uint16_t* h) {
+hipError_t launch_lds(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
+                      int splits) {
+  constexpr int WV = kGemmTileRows / 16;
   const int mb = mb_for(M);
   const int kslice = kslice_for(K, splits);
   const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  const dim3 grid((N + WV * 16 - 1) / (WV * 16), splits, mchunks);
+  const dim3 grid((N + kGemmTileRows - 1) / kGemmTileRows, splits, mchunks);
   const dim3 block(WV * 64);
-  const bf16x8_t* x = (const bf16x8_t*)X;
-  const bf16x8_t* w = (const bf16x8_t*)W;
   switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4, WV, SWI>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    case 8:
-      if constexpr (SWI) return hipErrorInvalidValue;
-      else hipLaunchKernelGGL((k_gemm_bf16<8, 4, WV, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
-      break;
-    default:
-      if constexpr (SWI) return hipErrorInvalidValue;
-      else hipLaunchKernelGGL((k_gemm_bf16<16, 2, WV, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
-      break;
+    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
+    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
+    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
+    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
+    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 4, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
+    default: hipLaunchKernelGGL((k_gemm_bf16<16, 2, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
+  }
+  return hipGetLastError();
+}
+
+// Ring kernel shape: weight blocks per wave and K splits, aiming at ~512 waves
+// with K slices of at least 256 (gate/up with SwiGLU: 4 blocks, one split).
+constexpr int kRingMaxRows = 64;
+constexpr int kRingTargetWaves = 512;
+int ring_splits(int N, int K, int max_splits) {
+  const int groups = (N / 16 + 7) / 8;
+  int s = (kRingTargetWaves + groups - 1) / groups;
+  s = std::min(s, std::max(1, K / 256));
+  s = std::max(1, std::min(s, max_splits));
+  const int ks = kslice_for(K, s);
+  return (K + ks - 1) / ks;
+}
+
+template <int NBW, bool SWI>
+hipError_t launch_ring(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
+                       int splits, uint16_t* h) {
+  const int kslice = kslice_for(K, splits);
+  const dim3 grid((N / 16 + NBW - 1) / NBW, splits);
+  switch ((M + 15) / 16) {
+    case 1: hipLaunchKernelGGL((k_gemm_ring<1, NBW, 2, SWI>), grid, dim3(64), 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 2: hipLaunchKernelGGL((k_gemm_ring<2, NBW, 2, SWI>), grid, dim3(64), 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 3: hipLaunchKernelGGL((k_gemm_ring<3, NBW, 2, SWI>), grid, dim3(64), 0, s, x, w, out, M, N, K, kslice, h); break;
+    default: hipLaunchKernelGGL((k_gemm_ring<4, NBW, 2, SWI>), grid, dim3(64), 0, s, x, w, out, M, N, K, kslice, h); break;
   }
   return hipGetLastError();
 }
@@ -215,6 +310,7 @@ hipError_t launch_bf16(hipStream_t s, const void* X, const void* W, float* out, 
 
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;
+  if (M <= kRingMaxRows) return ring_splits(N, K, max_splits);
   static const int target = env_int("ROLLOUT_GEMM_TARGET_WG", 768);
   static const int min_k = env_int("ROLLOUT_GEMM_MIN_KSLICE", 256);
   const int mb = mb_for(M);
@@ -236,16 +332,17 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
     hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, s, (const float*)X, ldx, (const float*)W, out, M, N, K);
     return hipGetLastError();
   }
-  return launch_bf16<kGemmTileRows / 16, false>(s, X, W, out, M, N, K, splits, nullptr);
+  if (N % 16 || K % 32) return hipErrorInvalidValue;
+  const bf16x8_t* x = (const bf16x8_t*)X;
+  const bf16x8_t* w = (const bf16x8_t*)W;
+  if (M <= kRingMaxRows) return launch_ring<8, false>(s, x, w, out, M, N, K, splits, nullptr);
+  return launch_lds(s, x, w, out, M, N, K, splits);
 }
 
 hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h) {
   if (M <= 0) return hipSuccess;
-  if (M > kSwigluMaxRows || N % 4) return hipErrorInvalidValue;
-  static const int wv = env_int("ROLLOUT_SWIGLU_WAVES", 4);
-  // 64-row workgroups: twice as many as 128-row ones, which balances the CUs better
-  if (wv == 8) return launch_bf16<8, true>(s, X, W, nullptr, M, N, K, 1, (uint16_t*)h);
-  return launch_bf16<4, true>(s, X, W, nullptr, M, N, K, 1, (uint16_t*)h);
+  if (M > kSwigluMaxRows || M > kRingMaxRows || N % 16 || K % 32) return hipErrorInvalidValue;
+  return launch_ring<4, true>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, 1, (uint16_t*)h);
 }
 
 }  // namespace rollout
