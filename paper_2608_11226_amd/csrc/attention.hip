@@ -56,58 +56,35 @@ struct KVTile {
   short4_t v[HD / 16];
 };
 
+// Loads one 16-token tile starting at tb.  Every load is issued unconditionally,
+// with rows past the context clamped onto its last token (they are masked when
+// the tile is used), so a wave can keep several tiles in flight without the
+// compiler draining the load queue.  Block ids come from the LDS copy of the
+// sequence's block table; an out-of-range id sets *bad and reads block 0.
 template <int HD>
-__device__ __forceinline__ void load_tile(KVTile<HD>& t, int tb, int t_end, int hh, int g, const int32_t* trow,
-                                          int blk, const uint16_t* kv, size_t block_stride, size_t layer_base,
-                                          size_t blk_elems, int n_blocks, int32_t* err) {
-  bf16x8_t zero8;
+__device__ __forceinline__ void load_tile(KVTile<HD>& t, int tb, int t_end, int hh, int g, const int* s_tab, int blk,
+                                          const uint16_t* kv, size_t block_stride, size_t layer_base,
+                                          size_t blk_elems, int n_blocks, bool* bad) {
+  const int tk = min(tb + hh, t_end - 1);            // key row supplied by this lane
+  const int tv = min(tb + 4 * g, (t_end - 1) & ~3);  // four value tokens tv .. tv+3 (never straddle a block)
+  int bk = s_tab[tk / blk], bv = s_tab[tv / blk];
+  if ((unsigned)bk >= (unsigned)n_blocks) { *bad = true; bk = 0; }
+  if ((unsigned)bv >= (unsigned)n_blocks) { *bad = true; bv = 0; }
+  const uint16_t* kp = kv + (size_t)bk * block_stride + layer_base + (size_t)(tk % blk) * HD + 8 * g;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
-  const int tk = tb + hh;  // key row supplied by this lane
-  bool kok = false;
-  if (tk < t_end) {
-    const int b = trow[tk / blk];
-    if (b >= 0 && b < n_blocks) {
-      const uint16_t* kp = kv + (size_t)b * block_stride + layer_base + (size_t)(tk % blk) * HD + 8 * g;
+  for (int c = 0; c < HD / 32; ++c) t.k[c] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * c);
+  const uint16_t* vp = kv + (size_t)bv * block_stride + layer_base + blk_elems + (tv % blk);
 #pragma unroll
-      for (int c = 0; c < HD / 32; ++c) t.k[c] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * c);
-      kok = true;
-    } else {
-      atomicOr(err, 4);
-    }
-  }
-  if (!kok) {
-#pragma unroll
-    for (int c = 0; c < HD / 32; ++c) t.k[c] = zero8;
-  }
-  const int tv = tb + 4 * g;  // four value tokens tv .. tv+3 (never straddle a block)
-  int vmask = tv < t_end ? min(4, t_end - tv) : 0;
-  if (vmask > 0) {
-    const int b = trow[tv / blk];
-    if (b >= 0 && b < n_blocks) {
-      const uint16_t* vp = kv + (size_t)b * block_stride + layer_base + blk_elems + (tv % blk);
-#pragma unroll
-      for (int j = 0; j < HD / 16; ++j) t.v[j] = *reinterpret_cast<const short4_t*>(vp + (size_t)(16 * j + hh) * blk);
-    } else {
-      vmask = 0;
-    }
-  }
-  if (vmask < 4) {  // tokens past the context may hold stale data: never let them reach the MFMA
-#pragma unroll
-    for (int j = 0; j < HD / 16; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (e >= vmask) t.v[j][e] = 0;
-  }
+  for (int j = 0; j < HD / 16; ++j) t.v[j] = *reinterpret_cast<const short4_t*>(vp + (size_t)(16 * j + hh) * blk);
 }
 
 template <int HD>
-__device__ __forceinline__ void attend_tile(const KVTile<HD>& t, const bf16x8_t* qf, int tb, int t_end, int g,
-                                            float scale, float& m_run, float& l_run, floatx4_t* o) {
+__device__ __forceinline__ void attend_tile(KVTile<HD>& t, const bf16x8_t* qf, int tb, int t_end, int g, float scale,
+                                            float& m_run, float& l_run, floatx4_t* o) {
   floatx4_t s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int c = 0; c < HD / 32; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(t.k[c], qf[c], s, 0, 0, 0);
-  // s[i] = score of token tb + 4g + i for head lane%16
+  // s[i] = score of token tb + 4g + i for head lane%16; tokens past the context drop out here
   float mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -128,6 +105,14 @@ __device__ __forceinline__ void attend_tile(const KVTile<HD>& t, const bf16x8_t*
   ps += __shfl_xor(ps, 32, 64);
   l_run = l_run * alpha + ps;
   m_run = m_new;
+  if (tb + 16 > t_end) {  // the clamped rows of the last tile may hold stale data: keep them out of the MFMA
+    const int vm = t_end - (tb + 4 * g);
+#pragma unroll
+    for (int j = 0; j < HD / 16; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e >= vm) t.v[j][e] = 0;
+  }
   const short4_t pf = {f2bs(p[0]), f2bs(p[1]), f2bs(p[2]), f2bs(p[3])};
 #pragma unroll
   for (int j = 0; j < HD / 16; ++j) {
@@ -141,6 +126,9 @@ __device__ __forceinline__ void attend_tile(const KVTile<HD>& t, const bf16x8_t*
 // on q and k, bf16 rounding, k and v appended to the cache.  The current token
 // then enters the softmax as one more state beside the waves' states, so no
 // wave reads the cache entry this workgroup is writing.
+constexpr int kMaxQkvSplits = 16;  // most QKV split partials the attention kernel sums
+constexpr int kMaxTableBlocks = 16384;
+
 struct AttnQKV {
   const float* part;  // NULL: q is read from the q buffer and the cache already holds the current token
   int splits;
@@ -148,7 +136,7 @@ struct AttnQKV {
   const float* rope_sin;
 };
 
-template <int HD, int NW, bool FQ>
+template <int HD, int NW, int DR, bool FQ>
 __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
                                                        uint16_t* __restrict__ kv, int n_blocks,
                                                        const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
@@ -161,7 +149,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
   __shared__ float s_o[NW][16][HD + 4];
   __shared__ __align__(16) uint16_t s_q[FQ ? 16 : 1][HD];
   __shared__ float s_kv[FQ ? 2 : 1][HD];  // current token's k (rotated) and v, bf16 values
+  __shared__ __align__(16) float s_raw[FQ ? 18 : 1][HD];  // split sums: q heads, then k, then v
   __shared__ float s_cur[16];             // current token's scaled score per head
+  extern __shared__ int s_tab[];          // the sequence's block table (dynamic, max_blocks entries)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kvh = blockIdx.x % D.nkv;
   const int r = blockIdx.x / D.nkv;
@@ -180,14 +170,57 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
 #pragma unroll
   for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
 
+  int t_end = pos + 1;  // keys read from the cache
+  if constexpr (FQ) t_end = pos;
+  for (int i = tid; i < (t_end + blk - 1) / blk; i += NT) s_tab[i] = trow[i];
+  __syncthreads();
+
+  // wave w: tiles w, w + NW, ...  They pass through a ring of DR tiles in
+  // registers: while one is attended, the next DR - 1 are loading.  The first
+  // DR loads go out before q/k/v are formed, so they overlap that work.
+  constexpr int STRIDE = 16 * NW;
+  const int first = 16 * wave;
+  const int n_w = t_end > first ? (t_end - first + STRIDE - 1) / STRIDE : 0;
+  bool bad = false;
+  KVTile<HD> ring[DR];
+  if (n_w > 0) {
+#pragma unroll
+    for (int d = 0; d < DR; ++d) {
+      load_tile<HD>(ring[d], first + STRIDE * min(d, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride, layer_base,
+                    blk_elems, n_blocks, &bad);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
   // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
   bf16x8_t qf[KC];
-  int t_end = pos + 1;  // keys read from the cache
   if constexpr (FQ) {
-    t_end = pos;
-    constexpr int half = HD / 2;
+    // sums of the split partials, one float4 column group per thread, every split's load in flight at once
     const size_t n = D.nqkv, ss = (size_t)R * n;
     const float* pr = Q.part + (size_t)r * n;
+    const int ng = (nrep + 2) * (HD / 4);
+    for (int gi = tid; gi < ng; gi += NT) {
+      const int slot = gi / (HD / 4), i4 = (gi % (HD / 4)) * 4;
+      const int c = (slot < nrep ? (kvh * nrep + slot) * HD : D.qd + (slot - nrep) * D.kvd + kvh * HD) + i4;
+      float4 v[kMaxQkvSplits];
+#pragma unroll
+      for (int sp = 0; sp < kMaxQkvSplits; ++sp)
+        v[sp] = *reinterpret_cast<const float4*>(pr + (size_t)min(sp, Q.splits - 1) * ss + c);
+      float4 acc = v[0];
+#pragma unroll
+      for (int sp = 1; sp < kMaxQkvSplits; ++sp) {
+        if (sp < Q.splits) {
+          acc.x += v[sp].x;
+          acc.y += v[sp].y;
+          acc.z += v[sp].z;
+          acc.w += v[sp].w;
+        }
+      }
+      *reinterpret_cast<float4*>(&s_raw[slot][i4]) = acc;
+    }
+    __syncthreads();
+    // rotary embedding of q and k, bf16 rounding, cache append of k and v
+    constexpr int half = HD / 2;
     const float* cs = Q.rope_cos + (size_t)pos * half;
     const float* sn = Q.rope_sin + (size_t)pos * half;
     const int b = trow[pos / blk];
@@ -197,12 +230,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
     for (int it = tid; it < npair + HD; it += NT) {
       if (it < npair) {
         const int h = it / half, i = it - h * half;
-        const int c = (h < nrep ? (kvh * nrep + h) * HD : D.qd + kvh * HD) + i;
-        float x1 = 0.f, x2 = 0.f;
-        for (int sp = 0; sp < Q.splits; ++sp) {
-          x1 += pr[sp * ss + c];
-          x2 += pr[sp * ss + c + half];
-        }
+        const float x1 = s_raw[h][i], x2 = s_raw[h][i + half];
         const uint16_t b1 = f32_to_bf16(x1 * cs[i] - x2 * sn[i]);
         const uint16_t b2 = f32_to_bf16(x2 * cs[i] + x1 * sn[i]);
         if (h < nrep) {
@@ -218,10 +246,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
         }
       } else {
         const int i = it - npair;
-        const int c = D.qd + D.kvd + kvh * HD + i;
-        float v = 0.f;
-        for (int sp = 0; sp < Q.splits; ++sp) v += pr[sp * ss + c];
-        const uint16_t bv = f32_to_bf16(v);
+        const uint16_t bv = f32_to_bf16(s_raw[nrep + 1][i]);
         s_kv[1][i] = bf16_to_f32(bv);
         if (bok) kdst[blk_elems + (size_t)i * blk + pos % blk] = bv;
       }
@@ -249,21 +274,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
 #pragma unroll
   for (int j = 0; j < DT; ++j) o[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  // wave w: tiles w, w + NW, ...; two tiles in registers, the next one loading while one is computed
-  constexpr int STRIDE = 16 * NW;
-  KVTile<HD> ta, tb_;
-  int t0 = 16 * wave;
-  if (t0 < t_end) load_tile<HD>(ta, t0, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
-  while (t0 < t_end) {
-    const int t1 = t0 + STRIDE;
-    if (t1 < t_end) load_tile<HD>(tb_, t1, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
-    attend_tile<HD>(ta, qf, t0, t_end, g, scale, m_run, l_run, o);
-    if (t1 >= t_end) break;
-    const int t2 = t1 + STRIDE;
-    if (t2 < t_end) load_tile<HD>(ta, t2, t_end, hh, g, trow, blk, kv, block_stride, layer_base, blk_elems, n_blocks, err);
-    attend_tile<HD>(tb_, qf, t1, t_end, g, scale, m_run, l_run, o);
-    t0 = t2;
+  if (n_w > 0) {
+    for (int i = 0; i < n_w; i += DR) {
+#pragma unroll
+      for (int d = 0; d < DR; ++d) {
+        if (i + d < n_w) attend_tile<HD>(ring[d], qf, first + STRIDE * (i + d), t_end, g, scale, m_run, l_run, o);
+        load_tile<HD>(ring[d], first + STRIDE * min(i + d + DR, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride,
+                      layer_base, blk_elems, n_blocks, &bad);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
   }
+  if (bad) atomicOr(err, 4);
 
   // merge the waves: o[j][i] is head hh at dimension 16 j + 4 g + i
   if (g == 0) {
@@ -444,6 +466,7 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ o
   st8(out, xoff(out, r, g * 8, qd, (R + 15) >> 4), o);
 }
 
+
 bool mfma_attention(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 && (D.hd == 128 || D.hd == 64); }
 
 }  // namespace
@@ -462,8 +485,10 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
                             int layer, float* opart, float* ml, void* out, int32_t* err, const float* qkv_part,
                             int qkv_splits, const float* rope_cos, const float* rope_sin) {
   if (R <= 0) return hipSuccess;
-  if (qkv_part && (!mfma_attention(D) || rm.P != 0)) return hipErrorInvalidValue;
+  if (qkv_part && (!mfma_attention(D) || rm.P != 0 || qkv_splits < 1 || qkv_splits > kMaxQkvSplits))
+    return hipErrorInvalidValue;
   if (mfma_attention(D)) {
+    if (max_blocks > kMaxTableBlocks) return hipErrorInvalidValue;  // the block table is staged in LDS
     static const int nw = [] {
       const char* v = std::getenv("ROLLOUT_ATTN_WAVES");
       const int w = v ? std::atoi(v) : 8;
@@ -474,9 +499,10 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
     const uint16_t* qq = (const uint16_t*)q;
     uint16_t* kk = (uint16_t*)kv_pool;
     uint16_t* oo = (uint16_t*)out;
-#define ROLLOUT_MFMA_ATTN(HD, NW, FQ)                                                                              \
-  hipLaunchKernelGGL((k_attn_mfma<HD, NW, FQ>), grid, dim3(NW * 64), 0, s, D, qq, kk, n_blocks, tables, max_blocks, rm, \
-                     R, layer, Q, oo, err)
+    const size_t tab_bytes = (size_t)max_blocks * 4;
+#define ROLLOUT_MFMA_ATTN(HD, NW, FQ)                                                                                 \
+  hipLaunchKernelGGL((k_attn_mfma<HD, NW, 2, FQ>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk, n_blocks, tables, \
+                     max_blocks, rm, R, layer, Q, oo, err)
 #define ROLLOUT_MFMA_ATTN_NW(HD, FQ)         \
   do {                                       \
     if (nw == 4) ROLLOUT_MFMA_ATTN(HD, 4, FQ); \
