@@ -150,6 +150,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
   __shared__ __align__(16) uint16_t s_q[FQ ? 16 : 1][HD];
   __shared__ float s_kv[FQ ? 2 : 1][HD];  // current token's k (rotated) and v, bf16 values
   __shared__ __align__(16) float s_raw[FQ ? 18 : 1][HD];  // split sums: q heads, then k, then v
+  __shared__ float s_rope[FQ ? HD : 1];                   // cos (first half), sin (second half) at pos
   __shared__ float s_cur[16];             // current token's scaled score per head
   extern __shared__ int s_tab[];          // the sequence's block table (dynamic, max_blocks entries)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -172,30 +173,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
 
   int t_end = pos + 1;  // keys read from the cache
   if constexpr (FQ) t_end = pos;
-  for (int i = tid; i < (t_end + blk - 1) / blk; i += NT) s_tab[i] = trow[i];
-  __syncthreads();
-
-  // wave w: tiles w, w + NW, ...  They pass through a ring of DR tiles in
-  // registers: while one is attended, the next DR - 1 are loading.  The first
-  // DR loads go out before q/k/v are formed, so they overlap that work.
-  constexpr int STRIDE = 16 * NW;
-  const int first = 16 * wave;
-  const int n_w = t_end > first ? (t_end - first + STRIDE - 1) / STRIDE : 0;
-  bool bad = false;
-  KVTile<HD> ring[DR];
-  if (n_w > 0) {
-#pragma unroll
-    for (int d = 0; d < DR; ++d) {
-      load_tile<HD>(ring[d], first + STRIDE * min(d, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride, layer_base,
-                    blk_elems, n_blocks, &bad);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
-
-  // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
-  bf16x8_t qf[KC];
+  // One round trip for everything that does not depend on the block table:
+  // the table itself, the row's rotary factors and the QKV split sums
+  // (one float4 column group per thread, every split's load in flight at once).
+  const int ntab = (t_end + blk - 1) / blk;
+  for (int i = tid; i < ntab; i += NT) s_tab[i] = trow[i];
   if constexpr (FQ) {
-    // sums of the split partials, one float4 column group per thread, every split's load in flight at once
+    constexpr int half = HD / 2;
+    if (tid < HD) s_rope[tid] = tid < half ? Q.rope_cos[(size_t)pos * half + tid] : Q.rope_sin[(size_t)pos * half + tid - half];
     const size_t n = D.nqkv, ss = (size_t)R * n;
     const float* pr = Q.part + (size_t)r * n;
     const int ng = (nrep + 2) * (HD / 4);
@@ -218,11 +203,33 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
       }
       *reinterpret_cast<float4*>(&s_raw[slot][i4]) = acc;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+
+  // wave w: tiles w, w + NW, ...  They pass through a ring of DR tiles in
+  // registers: while one is attended, the next DR - 1 are loading.  The first
+  // DR loads go out before q/k/v are rotated, so they overlap that work.
+  constexpr int STRIDE = 16 * NW;
+  const int first = 16 * wave;
+  const int n_w = t_end > first ? (t_end - first + STRIDE - 1) / STRIDE : 0;
+  bool bad = false;
+  KVTile<HD> ring[DR];
+  if (n_w > 0) {
+#pragma unroll
+    for (int d = 0; d < DR; ++d) {
+      load_tile<HD>(ring[d], first + STRIDE * min(d, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride, layer_base,
+                    blk_elems, n_blocks, &bad);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
+  bf16x8_t qf[KC];
+  if constexpr (FQ) {
     // rotary embedding of q and k, bf16 rounding, cache append of k and v
     constexpr int half = HD / 2;
-    const float* cs = Q.rope_cos + (size_t)pos * half;
-    const float* sn = Q.rope_sin + (size_t)pos * half;
+    const float* cs = s_rope;
+    const float* sn = s_rope + half;
     const int b = trow[pos / blk];
     const bool bok = b >= 0 && b < n_blocks;
     uint16_t* kdst = kv + (size_t)(bok ? b : 0) * block_stride + layer_base;
@@ -494,19 +501,26 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
       const int w = v ? std::atoi(v) : 8;
       return w == 4 ? 4 : 8;
     }();
+    static const int dr = [] {
+      const char* v = std::getenv("ROLLOUT_ATTN_RING");
+      const int d = v ? std::atoi(v) : 2;
+      return d == 3 || d == 4 ? d : 2;
+    }();
     const dim3 grid((unsigned)R * D.nkv);
     const AttnQKV Q{qkv_part, qkv_splits, rope_cos, rope_sin};
     const uint16_t* qq = (const uint16_t*)q;
     uint16_t* kk = (uint16_t*)kv_pool;
     uint16_t* oo = (uint16_t*)out;
     const size_t tab_bytes = (size_t)max_blocks * 4;
-#define ROLLOUT_MFMA_ATTN(HD, NW, FQ)                                                                                 \
-  hipLaunchKernelGGL((k_attn_mfma<HD, NW, 2, FQ>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk, n_blocks, tables, \
+#define ROLLOUT_MFMA_ATTN(HD, NW, DR, FQ)                                                                              \
+  hipLaunchKernelGGL((k_attn_mfma<HD, NW, DR, FQ>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk, n_blocks, tables, \
                      max_blocks, rm, R, layer, Q, oo, err)
-#define ROLLOUT_MFMA_ATTN_NW(HD, FQ)         \
-  do {                                       \
-    if (nw == 4) ROLLOUT_MFMA_ATTN(HD, 4, FQ); \
-    else ROLLOUT_MFMA_ATTN(HD, 8, FQ);       \
+#define ROLLOUT_MFMA_ATTN_NW(HD, FQ)                    \
+  do {                                                  \
+    if (nw == 4) ROLLOUT_MFMA_ATTN(HD, 4, 2, FQ);         \
+    else if (dr == 3) ROLLOUT_MFMA_ATTN(HD, 8, 3, FQ);    \
+    else if (dr == 4) ROLLOUT_MFMA_ATTN(HD, 8, 4, FQ);    \
+    else ROLLOUT_MFMA_ATTN(HD, 8, 2, FQ);                 \
   } while (0)
     if (D.hd == 128) {
       if (qkv_part) ROLLOUT_MFMA_ATTN_NW(128, true);

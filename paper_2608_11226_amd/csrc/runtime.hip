@@ -97,7 +97,10 @@ rollout_status validate_config(const rollout_model_config* c, std::string* msg) 
     *msg = "kv_block_size must be 8, 16 or 32";
     return ROLLOUT_EUNSUPPORTED;
   }
-  if ((int64_t)c->max_prompt_len + c->max_new_tokens > (1 << 20)) { *msg = "context longer than 2^20 tokens"; return ROLLOUT_EUNSUPPORTED; }
+  if (((int64_t)c->max_prompt_len + c->max_new_tokens + c->kv_block_size - 1) / c->kv_block_size > 16384) {
+    *msg = "context longer than 16384 KV blocks";  // the attention kernel stages a sequence's block table in LDS
+    return ROLLOUT_EUNSUPPORTED;
+  }
   if ((int64_t)c->vocab * c->d_model > ((int64_t)1 << 31) - 1 || (int64_t)c->d_ff * 2 * c->d_model > ((int64_t)1 << 31) - 1) {
     *msg = "a weight matrix exceeds 2^31 elements";
     return ROLLOUT_EUNSUPPORTED;
