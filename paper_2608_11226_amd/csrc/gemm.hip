@@ -24,11 +24,18 @@
 // that holds one also holds the other, and h goes straight to the down
 // projection's operand layout.
 //
-// k_gemm_bf16 (prefill and other batches above 64 rows): a workgroup of
-// eight waves owns 128 weight rows (16 per wave) and a K range; it stages X
-// through a double-buffered LDS slab shared by the eight waves (X is re-read
-// from L2 once per 128 weight rows), while the weights and the next slab are
-// in flight in registers; split partials as above.
+// k_gemm_tile (prefill and other batches above 64 rows): a workgroup of four
+// waves owns a 128 x 128 output tile (8 weight blocks x 8 activation blocks,
+// 64 x 64 per wave, 16 MFMAs per k-step from 8 LDS fragment reads).  Both
+// operands reach LDS by direct global-to-LDS loads, one 1 KB fragment per
+// wave instruction (the HBM layouts are already fragment order), into a
+// double buffer of two k-steps per stage; the wave waits for its own loads
+// with an explicit count and a barrier publishes the stage.  The loads are
+// written as inline asm so the compiler neither drains them at the barrier nor
+// orders LDS reads behind them; the explicit wait is what makes the stage
+// visible.  Workgroup order is XCD-aware: the M tiles of one N tile run on one
+// XCD, so its weight tile is fetched into that XCD's L2 once.  The inner loop
+// is bound by LDS bandwidth (fragment reads plus the loads' LDS writes).
 //
 // fp32 path: a plain LDS-tiled VALU GEMM over row-major X and W (the fp32
 // path exists for exact parity on small models, not for speed).
@@ -47,92 +54,104 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-// MB: 16-row blocks of X per workgroup pass; KS: k-steps (of 32) per staged X slab;
-// WV: waves per workgroup (16 weight rows each).
-template <int MB, int KS, int WV>
-__global__ __launch_bounds__(WV * 64) void k_gemm_bf16(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
-                                                       float* __restrict__ out, int M, int N, int K, int kslice) {
-  constexpr int NTH = WV * 64;
-  constexpr int XV = KS * MB * 64;  // 16-byte X vectors per slab
-  constexpr int XPT = (XV + NTH - 1) / NTH;
-  __shared__ bf16x8_t xs[2][XV];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nb = blockIdx.x * WV + wave;  // this wave's 16-row weight block
-  const bool nvalid = nb * 16 < N;
-  const int kbt = K >> 5;
-  const int Mb = (M + 15) >> 4;
-  const int kb0 = (int)(blockIdx.y * kslice) >> 5;
-  const int kb1 = min(kbt, kb0 + (kslice >> 5));
-  const int mb0 = blockIdx.z * MB;
-  const bf16x8_t* wp = W + (size_t)(nvalid ? nb : 0) * (size_t)kbt * 64 + lane;
+// s_waitcnt immediate that waits until at most n vector memory operations are outstanding
+constexpr int vm_wait(int n) { return (n & 0xF) | ((n & 0x30) << 10) | (0x7 << 4) | (0xF << 8); }
 
-  bf16x8_t zero;
+// KS k-steps per stage, NS stages in the LDS ring.
+template <int KS, int NS>
+__global__ __launch_bounds__(256) void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
+                                                   float* __restrict__ out, int M, int N, int K, int kslice) {
+  constexpr int FPW = 4 * KS;  // fragments each wave loads per stage (8 KS of W, 8 KS of X per workgroup)
+  __shared__ bf16x8_t lds[NS][2][8][KS][64];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int nbt = N >> 4, kbt = K >> 5, Mb = (M + 15) >> 4;
+  const int Mt = (Mb + 7) / 8, Nt = (nbt + 7) / 8;
+  // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD
+  const int b = blockIdx.x;
+  const int grp = b / (8 * Mt), rem = b % (8 * Mt);
+  const int nt = grp * 8 + rem % 8, mt = rem / 8;
+  if (nt >= Nt) return;
+  const int nb0 = nt * 8, mb0 = mt * 8;
+  const int kb0 = (int)blockIdx.y * (kslice >> 5);
+  const int nk = min(kbt, kb0 + (kslice >> 5)) - kb0;
+  const int nst = (nk + KS - 1) / KS;
+  floatx4_t acc[4][4];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) zero[e] = (__bf16)0.0f;
-  floatx4_t acc[MB];
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
-  bf16x8_t wcur[KS], wnxt[KS], xr[XPT];
-#define LOAD_W(dst, kb)                                               \
-  _Pragma("unroll") for (int ks = 0; ks < KS; ++ks) dst[ks] =         \
-      (nvalid && (kb) + ks < kb1) ? __builtin_nontemporal_load(wp + (size_t)((kb) + ks) * 64) : zero;
-#define LOAD_X(kb)                                                                      \
-  _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
-    const int v = tid + NTH * j;                                                        \
-    bf16x8_t t = zero;                                                                  \
-    if (v < XV) {                                                                       \
-      const int ks = v / (MB * 64), mb = (v >> 6) % MB, ln = v & 63;                    \
-      const int m = (mb0 + mb) * 16 + (ln & 15), kk = (kb) + ks;                        \
-      if (kk < kb1 && m < M) t = XF[((size_t)kk * Mb + mb0 + mb) * 64 + ln];            \
-    }                                                                                   \
-    xr[j] = t;                                                                          \
-  }
-#define STORE_X(buf)                                                                    \
-  _Pragma("unroll") for (int j = 0; j < XPT; ++j) {                                     \
-    const int v = tid + NTH * j;                                                        \
-    if (v < XV) xs[buf][v] = xr[j];                                                     \
-  }
-
-  LOAD_W(wcur, kb0);
-  LOAD_X(kb0);
-  STORE_X(0);
-  __syncthreads();
-  int buf = 0;
-  for (int kb = kb0; kb < kb1; kb += KS) {
-    const int kn = kb + KS;
-    const bool more = kn < kb1;
-    if (more) {
-      LOAD_W(wnxt, kn);
-      LOAD_X(kn);
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  if (nst > 0) {
+    // this wave's fragments of a stage: ids wave*FPW .. +FPW-1 over [W|X][block][k-step], clamped into range
+    const bf16x8_t* src[FPW];
+    uint32_t dst[FPW];
+    int fks[FPW];
+    bool fw[FPW];
+#pragma unroll
+    for (int f = 0; f < FPW; ++f) {
+      const int id = wave * FPW + f;
+      const int op = id / (8 * KS), blk = (id % (8 * KS)) / KS;
+      fks[f] = id % KS;
+      fw[f] = op == 0;
+      src[f] = op == 0 ? W + ((size_t)min(nb0 + blk, nbt - 1) * kbt + kb0) * 64 + lane
+                       : XF + ((size_t)kb0 * Mb + min(mb0 + blk, Mb - 1)) * 64 + lane;
+      dst[f] = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)&lds[0][op][blk][fks[f]][0];
     }
+    constexpr uint32_t kStageBytes = 2 * 8 * KS * 64 * 16;
+    auto issue = [&](int st) {  // stage st (past the end: reloads the last k-step, never computed)
+      const uint32_t base = (uint32_t)(st % NS) * kStageBytes;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (kb + ks < kb1) {
+      for (int f = 0; f < FPW; ++f) {
+        const int kk = min(st * KS + fks[f], nk - 1);
+        const bf16x8_t* p = src[f] + (size_t)kk * (fw[f] ? 64 : (size_t)Mb * 64);
+        // M0 holds the LDS destination; it is restored, and one wait state separates its write from the load
+        int saved;
+        asm volatile(
+            "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+            : "=&s"(saved)
+            : "v"(p), "s"(__builtin_amdgcn_readfirstlane(dst[f] + base))
+            : "memory");
+      }
+    };
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks], xs[buf][(ks * MB + mb) * 64 + lane], acc[mb],
-                                                            0, 0, 0);
+    for (int s0 = 0; s0 < NS - 1; ++s0) issue(s0);
+    for (int st = 0; st < nst; ++st) {
+      __builtin_amdgcn_s_waitcnt(vm_wait((NS - 2) * FPW));  // this wave's loads of stage st have landed
+      __syncthreads();                                      // ... and every wave's; stage st - 1 is free
+      issue(st + NS - 1);
+      const int slot = st % NS;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (st * KS + ks < nk) {
+          bf16x8_t wf[4], xf[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) wf[i] = lds[slot][0][4 * wn + i][ks][lane];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) xf[j] = lds[slot][1][4 * wm + j][ks][lane];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], xf[j], acc[i][j], 0, 0, 0);
+        }
       }
     }
-    if (more) STORE_X(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) wcur[ks] = wnxt[ks];
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));  // no load may still be writing LDS when the workgroup ends
   }
-#undef LOAD_W
-#undef LOAD_X
-#undef STORE_X
-  if (!nvalid) return;
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
-  const int n = nb * 16 + 4 * (lane >> 4);
-  float* o = out + (size_t)blockIdx.y * (size_t)M * (size_t)N;
+  float* o = out + (size_t)blockIdx.y * M * N;
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int m = (mb0 + mb) * 16 + (lane & 15);
-    if (m < M)
-      *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]);
+  for (int i = 0; i < 4; ++i) {
+    const int nb = nb0 + 4 * wn + i;
+    if (nb >= nbt) continue;
+    const int n = nb * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int m = (mb0 + 4 * wm + j) * 16 + (lane & 15);
+      if (m < M)
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    }
   }
 }
 
@@ -242,14 +261,6 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   if (m < M && n < N) out[(size_t)m * N + n] = acc;
 }
 
-// m-blocks of 16 rows handled by one workgroup pass
-int mb_for(int M) {
-  const int mb = (M + 15) / 16;
-  if (mb <= 4) return mb;
-  if (mb <= 8) return 8;
-  return 16;
-}
-
 int env_int(const char* name, int dflt) {
   const char* v = std::getenv(name);
   return v ? std::atoi(v) : dflt;
@@ -260,22 +271,16 @@ int kslice_for(int K, int splits) {
   return (per + 31) / 32 * 32;
 }
 
-hipError_t launch_lds(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
-                      int splits) {
-  constexpr int WV = kGemmTileRows / 16;
-  const int mb = mb_for(M);
-  const int kslice = kslice_for(K, splits);
-  const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  const dim3 grid((N + kGemmTileRows - 1) / kGemmTileRows, splits, mchunks);
-  const dim3 block(WV * 64);
-  switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemm_bf16<1, 8, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
-    case 2: hipLaunchKernelGGL((k_gemm_bf16<2, 8, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
-    case 3: hipLaunchKernelGGL((k_gemm_bf16<3, 4, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
-    case 4: hipLaunchKernelGGL((k_gemm_bf16<4, 4, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
-    case 8: hipLaunchKernelGGL((k_gemm_bf16<8, 4, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
-    default: hipLaunchKernelGGL((k_gemm_bf16<16, 2, WV>), grid, block, 0, s, x, w, out, M, N, K, kslice); break;
-  }
+// Tile kernel grid: (padded N tiles) x (M tiles) workgroups in XCD-aware order, K splits in y.
+int tile_groups(int M, int N) {
+  const int Mt = ((M + 15) / 16 + 7) / 8, Nt = (N / 16 + 7) / 8;
+  return (Nt + 7) / 8 * 8 * Mt;
+}
+
+hipError_t launch_tile(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
+                       int splits) {
+  const dim3 grid(tile_groups(M, N), splits);
+  hipLaunchKernelGGL((k_gemm_tile<2, 2>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice_for(K, splits));
   return hipGetLastError();
 }
 
@@ -311,15 +316,11 @@ hipError_t launch_ring(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, floa
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;
   if (M <= kRingMaxRows) return ring_splits(N, K, max_splits);
-  static const int target = env_int("ROLLOUT_GEMM_TARGET_WG", 768);
-  static const int min_k = env_int("ROLLOUT_GEMM_MIN_KSLICE", 256);
-  const int mb = mb_for(M);
-  const int mchunks = ((M + 15) / 16 + mb - 1) / mb;
-  const int nwg = (N + kGemmTileRows - 1) / kGemmTileRows * mchunks;
-  int s = (target + nwg - 1) / nwg;
-  s = std::min(s, std::max(1, K / min_k));
-  s = std::min(s, max_splits);
-  s = std::max(s, 1);
+  // tile kernel: enough K splits for ~2 workgroups per CU, K slices of at least 512
+  const int nwg = (((M + 15) / 16 + 7) / 8) * ((N / 16 + 7) / 8);
+  int s = (512 + nwg - 1) / nwg;
+  s = std::min(s, std::max(1, K / 512));
+  s = std::max(1, std::min(s, max_splits));
   const int ks = kslice_for(K, s);
   return (K + ks - 1) / ks;
 }
@@ -336,7 +337,7 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
   const bf16x8_t* x = (const bf16x8_t*)X;
   const bf16x8_t* w = (const bf16x8_t*)W;
   if (M <= kRingMaxRows) return launch_ring<8, false>(s, x, w, out, M, N, K, splits, nullptr);
-  return launch_lds(s, x, w, out, M, N, K, splits);
+  return launch_tile(s, x, w, out, M, N, K, splits);
 }
 
 hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h) {

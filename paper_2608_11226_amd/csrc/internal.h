@@ -70,7 +70,6 @@ int gemm_splits(int dtype, int M, int N, int K, int max_splits);
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const void* W, float* out, int M,
                        int N, int K, int splits);
 
-constexpr int kGemmTileRows = 128;  // weight rows (output columns) per workgroup of the split-K kernel
 // Decode gate/up projection with SwiGLU applied to its own output (bf16, one
 // K split, M <= kSwigluMaxRows): W holds gate row i at physical row 2i and up
 // row i at 2i + 1; h[m][i] = silu(gate) * up in the down projection's operand layout.
