@@ -134,9 +134,15 @@ struct AttnQKV {
   int splits;
   const float* rope_cos;
   const float* rope_sin;
+  // shared-prefix decode (see k_attn_prefix): keys before t_begin are left to the prefix kernel, the
+  // rotated q is kept in q_keep, and the unnormalised softmax state goes to st_o / st_ml
+  int t_begin;
+  uint16_t* q_keep;
+  float* st_o;   // [row][head][HD]: sum of p * v relative to the state's max
+  float* st_ml;  // [row][head][2]: max, sum of p
 };
 
-template <int HD, int NW, int DR, bool FQ>
+template <int HD, int NW, int DR, bool FQ, bool SPLIT = false>
 __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
                                                        uint16_t* __restrict__ kv, int n_blocks,
                                                        const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
@@ -210,7 +216,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
   // registers: while one is attended, the next DR - 1 are loading.  The first
   // DR loads go out before q/k/v are rotated, so they overlap that work.
   constexpr int STRIDE = 16 * NW;
-  const int first = 16 * wave;
+  const int first = (SPLIT ? Q.t_begin : 0) + 16 * wave;
   const int n_w = t_end > first ? (t_end - first + STRIDE - 1) / STRIDE : 0;
   bool bad = false;
   KVTile<HD> ring[DR];
@@ -243,6 +249,11 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
         if (h < nrep) {
           s_q[h][i] = b1;
           s_q[h][i + half] = b2;
+          if constexpr (SPLIT) {
+            uint16_t* qk = Q.q_keep + (size_t)r * D.qd + (size_t)(kvh * nrep + h) * HD;
+            qk[i] = b1;
+            qk[i + half] = b2;
+          }
         } else {
           s_kv[0][i] = bf16_to_f32(b1);
           s_kv[0][i + half] = bf16_to_f32(b2);
@@ -328,10 +339,148 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
 #pragma unroll
       for (int e = 0; e < 8; ++e) num[e] += wt * s_kv[1][d0 + e];
     }
+    if constexpr (SPLIT) {
+      const size_t hr = (size_t)r * D.nh + kvh * nrep + h;
+      float4* so = reinterpret_cast<float4*>(Q.st_o + hr * HD + d0);
+      so[0] = make_float4(num[0], num[1], num[2], num[3]);
+      so[1] = make_float4(num[4], num[5], num[6], num[7]);
+      if (d0 == 0) {
+        Q.st_ml[hr * 2] = mx;
+        Q.st_ml[hr * 2 + 1] = den;
+      }
+    } else {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = den > 0.f ? num[e] / den : 0.f;
+      st8(out, xoff(out, r, (kvh * nrep + h) * HD + d0, D.qd, Mb), v);
+    }
+  }
+}
+
+// Shared-prefix (group-aware) decode attention.  The G sequences of a group
+// share the physical KV blocks of their prompt's full blocks, tokens
+// [0, p_shared).  One workgroup per (group, KV head, block of 16 query
+// columns), a column being one (sequence, query head) pair of the group, reads
+// each shared K/V tile once for all 16 columns (the workgroups of one group and
+// KV head are placed on one XCD, so their tile reads meet in its L2), merges
+// its waves' softmax states with the state the suffix pass left for the
+// column (keys p_shared .. pos, current token included) and writes the
+// normalised output in the O-projection operand layout.
+template <int HD, int NW, int DR>
+__global__ __launch_bounds__(NW * 64) void k_attn_prefix(Dims D, const uint16_t* __restrict__ q,
+                                                         const uint16_t* __restrict__ kv, int n_blocks,
+                                                         const int32_t* __restrict__ tables, int max_blocks,
+                                                         int layer, int seq0, int G, int n_groups, int p_shared,
+                                                         const float* __restrict__ st_o,
+                                                         const float* __restrict__ st_ml, int R,
+                                                         uint16_t* __restrict__ out, int32_t* __restrict__ err) {
+  constexpr int KC = HD / 32, DT = HD / 16, NT = NW * 64;
+  __shared__ float s_m[NW][16], s_l[NW][16];
+  __shared__ float s_o[NW][16][HD + 4];
+  extern __shared__ int s_tab[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nrep = D.nh / D.nkv;
+  const int QB = (G * nrep + 15) / 16;
+  // workgroup order: the QB column blocks of one (group, KV head) share an XCD (workgroup b runs on XCD b % 8)
+  const int b = blockIdx.x;
+  const int gk = (b / (8 * QB)) * 8 + b % 8, qb = (b / 8) % QB;
+  if (gk >= n_groups * D.nkv) return;
+  const int grp = gk / D.nkv, kvh = gk % D.nkv;
+  const int hh = lane & 15, g = lane >> 4;
+  const int blk = D.blk;
+  const size_t blk_elems = (size_t)blk * HD;
+  const size_t kv_head_stride = 2 * blk_elems;
+  const size_t layer_base = ((size_t)layer * D.nkv + kvh) * kv_head_stride;
+  const size_t block_stride = (size_t)D.L * D.nkv * kv_head_stride;
+  const int32_t* trow = tables + (size_t)(seq0 + grp * G) * max_blocks;
+  for (int i = tid; i < p_shared / blk; i += NT) s_tab[i] = trow[i];
+  // this lane's query column: (row grp*G + c / nrep, head kvh*nrep + c % nrep)
+  const int c = 16 * qb + hh;
+  const bool cval = c < G * nrep;
+  const int row = grp * G + (cval ? c / nrep : 0), head = kvh * nrep + (cval ? c % nrep : 0);
+  bf16x8_t qf[KC];
+  {
+    bf16x8_t zero8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) zero8[e] = (__bf16)0.0f;
+    const uint16_t* qrow = q + (size_t)row * D.qd + (size_t)head * HD;
+#pragma unroll
+    for (int cc = 0; cc < KC; ++cc) qf[cc] = cval ? *reinterpret_cast<const bf16x8_t*>(qrow + 32 * cc + 8 * g) : zero8;
+  }
+  __syncthreads();
+  const float scale = 1.0f / sqrtf((float)HD);
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx4_t o[DT];
+#pragma unroll
+  for (int j = 0; j < DT; ++j) o[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  constexpr int STRIDE = 16 * NW;
+  const int first = 16 * wave;
+  const int t_end = p_shared;
+  const int n_w = t_end > first ? (t_end - first + STRIDE - 1) / STRIDE : 0;
+  bool bad = false;
+  if (n_w > 0) {
+    KVTile<HD> ring[DR];
+#pragma unroll
+    for (int d = 0; d < DR; ++d) {
+      load_tile<HD>(ring[d], first + STRIDE * min(d, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride, layer_base,
+                    blk_elems, n_blocks, &bad);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int i = 0; i < n_w; i += DR) {
+#pragma unroll
+      for (int d = 0; d < DR; ++d) {
+        if (i + d < n_w) attend_tile<HD>(ring[d], qf, first + STRIDE * (i + d), t_end, g, scale, m_run, l_run, o);
+        load_tile<HD>(ring[d], first + STRIDE * min(i + d + DR, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride,
+                      layer_base, blk_elems, n_blocks, &bad);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  if (bad) atomicOr(err, 4);
+  if (g == 0) {
+    s_m[wave][hh] = m_run;
+    s_l[wave][hh] = l_run;
+  }
+#pragma unroll
+  for (int j = 0; j < DT; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s_o[wave][hh][16 * j + 4 * g + i] = o[j][i];
+  __syncthreads();
+  // each thread finishes 8 consecutive dimensions of one column, merging the suffix state
+  const int Mb = (R + 15) >> 4;
+  for (int item = tid; item < 16 * (HD / 8); item += NT) {
+    const int cl = item / (HD / 8), d0 = (item % (HD / 8)) * 8;
+    const int cc = 16 * qb + cl;
+    if (cc >= G * nrep) continue;
+    const int rr = grp * G + cc / nrep, hd_ = kvh * nrep + cc % nrep;
+    const size_t hr = (size_t)rr * D.nh + hd_;
+    const float sm = st_ml[hr * 2], sl = st_ml[hr * 2 + 1];
+    float mx = sl > 0.f ? sm : -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      if (s_l[w][cl] > 0.f) mx = fmaxf(mx, s_m[w][cl]);
+    float num[8], den = 0.f;
+    {
+      const float wt = sl > 0.f ? expf(sm - mx) : 0.f;
+      const float4* so = reinterpret_cast<const float4*>(st_o + hr * HD + d0);
+      const float4 a0 = so[0], a1 = so[1];
+      den = wt * sl;
+      num[0] = wt * a0.x; num[1] = wt * a0.y; num[2] = wt * a0.z; num[3] = wt * a0.w;
+      num[4] = wt * a1.x; num[5] = wt * a1.y; num[6] = wt * a1.z; num[7] = wt * a1.w;
+    }
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      if (s_l[w][cl] > 0.f) {
+        const float wt = expf(s_m[w][cl] - mx);
+        den += wt * s_l[w][cl];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) num[e] += wt * s_o[w][cl][d0 + e];
+      }
+    }
     float v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = den > 0.f ? num[e] / den : 0.f;
-    st8(out, xoff(out, r, (kvh * nrep + h) * HD + d0, D.qd, Mb), v);
+    st8(out, xoff(out, rr, hd_ * HD + d0, D.qd, Mb), v);
   }
 }
 
@@ -478,6 +627,68 @@ bool mfma_attention(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 && (D.
 
 }  // namespace
 
+// Waves per decode-attention workgroup: eight when the grid is about one workgroup per CU (more loads in
+// flight per CU), four when there are at least two workgroups per CU to overlap each one's fixed phases
+// (q/k/v formation, merge) with the others' streaming.
+// ROLLOUT_ATTN_WAVES=4 or 8 forces the choice (read per call).
+int attn_waves(int n_workgroups) {
+  const char* v = std::getenv("ROLLOUT_ATTN_WAVES");
+  const int forced = v ? std::atoi(v) : 0;
+  if (forced == 4 || forced == 8) return forced;
+  return n_workgroups >= 512 ? 4 : 8;
+}
+
+bool attention_shares_prefix(const Dims& D) { return mfma_attention(D); }
+
+hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, int n_blocks, const int32_t* tables,
+                                   int max_blocks, RowMap rm, int R, int layer, int G, int p_shared, void* q_keep,
+                                   float* st_o, float* st_ml, void* out, int32_t* err, const float* qkv_part,
+                                   int qkv_splits, const float* rope_cos, const float* rope_sin) {
+  if (R <= 0) return hipSuccess;
+  if (!mfma_attention(D) || rm.P != 0 || G < 1 || R % G || p_shared < D.blk || p_shared % D.blk ||
+      qkv_splits < 1 || qkv_splits > kMaxQkvSplits || max_blocks > kMaxTableBlocks)
+    return hipErrorInvalidValue;
+  const AttnQKV Q{qkv_part, qkv_splits, rope_cos, rope_sin, p_shared, (uint16_t*)q_keep, st_o, st_ml};
+  uint16_t* kk = (uint16_t*)kv_pool;
+  uint16_t* oo = (uint16_t*)out;
+  // suffix: keys p_shared .. pos of every row, q/k/v formed, state kept
+  const size_t tab_bytes = (size_t)max_blocks * 4;
+  const dim3 sgrid((unsigned)R * D.nkv);
+#define ROLLOUT_SUFFIX(HD, NW)                                                                                       \
+  hipLaunchKernelGGL((k_attn_mfma<HD, NW, 2, true, true>), sgrid, dim3(NW * 64), tab_bytes, s, D,                     \
+                     (const uint16_t*)nullptr, kk, n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err)
+  const int nws = attn_waves(R * D.nkv);
+  if (D.hd == 128) {
+    if (nws == 4) ROLLOUT_SUFFIX(128, 4);
+    else ROLLOUT_SUFFIX(128, 8);
+  } else {
+    if (nws == 4) ROLLOUT_SUFFIX(64, 4);
+    else ROLLOUT_SUFFIX(64, 8);
+  }
+#undef ROLLOUT_SUFFIX
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // prefix: the group's shared prompt blocks once per (group, KV head, 16 query columns), then the merge
+  const int n_groups = R / G, nrep = D.nh / D.nkv, QB = (G * nrep + 15) / 16;
+  const int gk = n_groups * D.nkv;
+  const dim3 grid((unsigned)((gk + 7) / 8 * 8 * QB));
+  const size_t ptab = (size_t)(p_shared / D.blk) * 4;
+#define ROLLOUT_PREFIX(HD, NW)                                                                                       \
+  hipLaunchKernelGGL((k_attn_prefix<HD, NW, 2>), grid, dim3(NW * 64), ptab, s, D, (const uint16_t*)q_keep,           \
+                     (const uint16_t*)kv_pool, n_blocks, tables, max_blocks, layer, rm.seq0, G, n_groups, p_shared, \
+                     (const float*)st_o, (const float*)st_ml, R, oo, err)
+  const int nwp = attn_waves(gk * QB);
+  if (D.hd == 128) {
+    if (nwp == 4) ROLLOUT_PREFIX(128, 4);
+    else ROLLOUT_PREFIX(128, 8);
+  } else {
+    if (nwp == 4) ROLLOUT_PREFIX(64, 4);
+    else ROLLOUT_PREFIX(64, 8);
+  }
+#undef ROLLOUT_PREFIX
+  return hipGetLastError();
+}
+
 int attn_splits(int max_ctx, int* split_tokens) {
   const int st = 256;
   *split_tokens = st;
@@ -496,18 +707,14 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
     return hipErrorInvalidValue;
   if (mfma_attention(D)) {
     if (max_blocks > kMaxTableBlocks) return hipErrorInvalidValue;  // the block table is staged in LDS
-    static const int nw = [] {
-      const char* v = std::getenv("ROLLOUT_ATTN_WAVES");
-      const int w = v ? std::atoi(v) : 8;
-      return w == 4 ? 4 : 8;
-    }();
+    const int nw = attn_waves(R * D.nkv);
     static const int dr = [] {
       const char* v = std::getenv("ROLLOUT_ATTN_RING");
       const int d = v ? std::atoi(v) : 2;
       return d == 3 || d == 4 ? d : 2;
     }();
     const dim3 grid((unsigned)R * D.nkv);
-    const AttnQKV Q{qkv_part, qkv_splits, rope_cos, rope_sin};
+    const AttnQKV Q{qkv_part, qkv_splits, rope_cos, rope_sin, 0, nullptr, nullptr, nullptr};
     const uint16_t* qq = (const uint16_t*)q;
     uint16_t* kk = (uint16_t*)kv_pool;
     uint16_t* oo = (uint16_t*)out;

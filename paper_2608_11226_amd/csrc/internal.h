@@ -96,6 +96,15 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
                             const int32_t* tables, int max_blocks, RowMap rm, int R, int splits, int split_tokens,
                             int layer, float* opart, float* ml, void* out, int32_t* err, const float* qkv_part,
                             int qkv_splits, const float* rope_cos, const float* rope_sin);
+// Decode attention with the group's shared prompt read once per group: a suffix pass over each row's own
+// keys (p_shared .. pos; q/k/v formed from the QKV split partials as above, rotated q kept in q_keep,
+// softmax state in st_o [R][nh][hd] / st_ml [R][nh][2]) and a prefix pass over the shared blocks that
+// merges the state and writes out.  Rows are R / G whole groups in sequence order from rm.seq0.
+bool attention_shares_prefix(const Dims& D);
+hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, int n_blocks, const int32_t* tables,
+                                   int max_blocks, RowMap rm, int R, int layer, int G, int p_shared, void* q_keep,
+                                   float* st_o, float* st_ml, void* out, int32_t* err, const float* qkv_part,
+                                   int qkv_splits, const float* rope_cos, const float* rope_sin);
 hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
                               void* dst);
 hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);

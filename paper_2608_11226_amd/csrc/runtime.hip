@@ -10,6 +10,7 @@
 // every call, never state fixed at initialisation.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -302,6 +303,18 @@ rollout_status gemm_swiglu(rollout_ctx* c, const void* X, const void* W, int M, 
   return ROLLOUT_OK;
 }
 
+// Whether a decode batch takes the shared-prefix attention (whole groups of G >= 2 sequences whose prompt
+// fills at least one KV block).  By default only when G x shared prompt tokens >= 8192: below that the
+// group's redundant prompt reads are served by the caches and the extra pass costs more than it saves.
+// ROLLOUT_SHARED_PREFIX=0 never takes it, =2 always does (read per call).
+bool use_shared_prefix(const rollout_ctx* c, int M, const RowMap& rm) {
+  const char* v = std::getenv("ROLLOUT_SHARED_PREFIX");
+  const int mode = v ? std::atoi(v) : 1;
+  const int p_shared = c->P / c->D.blk * c->D.blk;
+  if (mode == 0 || !c->wave || c->G < 2 || p_shared < c->D.blk || M % c->G || rm.seq0 % c->G) return false;
+  return mode == 2 || (int64_t)c->G * p_shared >= 8192;
+}
+
 // One transformer pass over M rows (prefill chunk or decode batch). On return
 // c->Lo.a holds the final-normed hidden states (cache dtype).
 rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max, double kv_tokens_read) {
@@ -326,6 +339,8 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
     HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, nullptr, 1, M, D.d, x, c->at<float>(Lo.layers[0].attn_norm),
                                     D.eps, a), "rmsnorm");
   }
+  // decode rows of whole groups read their group's shared prompt blocks once per group (shared-prefix attention)
+  const int p_shared = (rm.P == 0 && attention_shares_prefix(D) && use_shared_prefix(c, M, rm)) ? c->P / D.blk * D.blk : 0;
   for (int l = 0; l < D.L; ++l) {
     const Layer& y = Lo.layers[l];
     int s;
@@ -341,9 +356,14 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
     {
       const double kvb = kv_tokens_read * D.nkv * 2.0 * D.hd * eb;
       Scope sc(c, 1, kvb + (double)M * D.qd * (eb + eb), 4.0 * kv_tokens_read * D.nh * D.hd);
-      HIP_TRY(c, launch_attention(c->stream, D, q, kv, c->n_blocks, tables, Lo.max_blocks, rm, M, asplits, st_tok, l,
-                                  opart, ml, o, err, attn_qkv ? part : nullptr, s, c->at<float>(Lo.rope_cos),
-                                  c->at<float>(Lo.rope_sin)), "attention");
+      if (attn_qkv && p_shared > 0)
+        HIP_TRY(c, launch_attention_shared(c->stream, D, kv, c->n_blocks, tables, Lo.max_blocks, rm, M, l, c->G,
+                                           p_shared, q, opart, ml, o, err, part, s, c->at<float>(Lo.rope_cos),
+                                           c->at<float>(Lo.rope_sin)), "attention");
+      else
+        HIP_TRY(c, launch_attention(c->stream, D, q, kv, c->n_blocks, tables, Lo.max_blocks, rm, M, asplits, st_tok, l,
+                                    opart, ml, o, err, attn_qkv ? part : nullptr, s, c->at<float>(Lo.rope_cos),
+                                    c->at<float>(Lo.rope_sin)), "attention");
     }
     r = gemm(c, o, c->at(y.wo), part, M, D.d, D.qd, kMaxSplits, &s);
     if (r) return r;

@@ -198,9 +198,24 @@ def test_generate_is_deterministic():
 # ---------------------------------------------------------------------------
 # bf16 path on a small GQA model
 # ---------------------------------------------------------------------------
+# Decode-attention path switches (read by the library per call): the shared-prefix pass (0 never, 1 by
+# size, 2 always) and the waves per attention workgroup (4 or 8; unset = by grid size).
+ATTN_KNOBS = [("1", None), ("2", "8"), ("2", "4"), ("0", "4")]
+
+
+def set_attn_knobs(monkeypatch, shared, waves):
+    monkeypatch.setenv("ROLLOUT_SHARED_PREFIX", shared)
+    if waves is None:
+        monkeypatch.delenv("ROLLOUT_ATTN_WAVES", raising=False)
+    else:
+        monkeypatch.setenv("ROLLOUT_ATTN_WAVES", waves)
+
+
+@pytest.mark.parametrize("shared,waves", ATTN_KNOBS)
 @pytest.mark.parametrize("n_prompts,G,P", [(3, 4, 32), (1, 16, 48), (5, 1, 20)])
-def test_bf16_small_teacher_forced_logits(n_prompts, G, P):
-    log(f"bf16 small GQA teacher forced prompts={n_prompts} G={G} P={P}")
+def test_bf16_small_teacher_forced_logits(n_prompts, G, P, shared, waves, monkeypatch):
+    set_attn_knobs(monkeypatch, shared, waves)
+    log(f"bf16 small GQA teacher forced prompts={n_prompts} G={G} P={P} shared={shared} waves={waves}")
     N = 8
     S = n_prompts * G
     cfg = R.model_config(SMALL_BF16, R.DTYPE_BF16, 64, N, S)
@@ -225,9 +240,11 @@ def test_bf16_small_teacher_forced_logits(n_prompts, G, P):
 GQA7_BF16 = (2, 256, 14, 2, 128, 512, 2048, 1e6)  # 7 query heads per KV head, head_dim 128 (the 7B ratio)
 
 
+@pytest.mark.parametrize("shared,waves", ATTN_KNOBS)
 @pytest.mark.parametrize("blk,n_prompts,G,P", [(16, 2, 8, 40), (8, 3, 2, 37), (32, 1, 4, 70), (16, 9, 1, 33)])
-def test_bf16_gqa7_teacher_forced_logits(blk, n_prompts, G, P):
-    log(f"bf16 GQA 14/2 x 128 teacher forced blk={blk} prompts={n_prompts} G={G} P={P}")
+def test_bf16_gqa7_teacher_forced_logits(blk, n_prompts, G, P, shared, waves, monkeypatch):
+    set_attn_knobs(monkeypatch, shared, waves)
+    log(f"bf16 GQA 14/2 x 128 teacher forced blk={blk} prompts={n_prompts} G={G} P={P} shared={shared} waves={waves}")
     N = 6
     S = n_prompts * G
     cfg = R.model_config(GQA7_BF16, R.DTYPE_BF16, 80, N, S, kv_block_size=blk)
@@ -247,6 +264,33 @@ def test_bf16_gqa7_teacher_forced_logits(blk, n_prompts, G, P):
     log(f"  max abs logit error per step: {[round(e, 5) for e in err]}")
     assert max(err) <= 3e-2
     eng.close()
+
+
+def test_bf16_gqa7_large_batch_teacher_forced_logits(monkeypatch):
+    # 32 groups of 8: 512 (row, KV head) attention workgroups, where the library picks four waves by itself;
+    # G x shared prompt = 8 x 64 keeps the shared-prefix pass off by size, so it is forced on here as well
+    for shared in ("1", "2"):
+        set_attn_knobs(monkeypatch, shared, None)
+        log(f"bf16 GQA 14/2 x 128 teacher forced, 32 prompts x G=8, P=70, shared={shared}")
+        n_prompts, G, P, N = 32, 8, 70, 3
+        S = n_prompts * G
+        cfg = R.model_config(GQA7_BF16, R.DTYPE_BF16, 80, N, S)
+        eng = R.Engine(cfg)
+        model = OracleModel(shape_of(cfg), mode="bf16")
+        prompts = W.prompts(n_prompts, P, cfg.vocab, seed=43)
+        u = W.uniforms(S, N, seed=44)
+        ref = rollout(model, prompts, G, N, 1.0, 1.0, u)
+        logits = torch.empty((S, cfg.vocab), dtype=torch.float32, device="cuda:0")
+        R.rollout_prefill(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, logits)
+        eng.synchronize()
+        err = [float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][0])))]
+        for t in range(1, N):
+            R.rollout_decode_step(eng.ctx, to_dev(ref["tokens"][:, t - 1], torch), logits)
+            eng.synchronize()
+            err.append(float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][t]))))
+        log(f"  max abs logit error per step: {[round(e, 5) for e in err]}")
+        assert max(err) <= 3e-2
+        eng.close()
 
 
 def test_device_error_flag_on_bad_token():
