@@ -25,6 +25,8 @@ excess), hand-traced hysteresis sequences, and the paper's own calibration figur
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 
 LEVELS = (1, 2, 4, 8)
@@ -37,7 +39,7 @@ def rolling_mean(p, dt: float, window_s: float) -> np.ndarray:
     out = np.empty_like(p)
     for i in range(len(p)):
         lo = max(0, i - k + 1)
-        out[i] = p[lo:i + 1].sum() / (i + 1 - lo)
+        out[i] = math.fsum(p[lo:i + 1]) / (i + 1 - lo)  # correctly rounded window sum
     return out
 
 
@@ -50,7 +52,7 @@ def violation_rate(p30, budget_w: float) -> float:
 def integrated_excess(p30, budget_w: float, dt: float) -> float:
     """Eq. (3): watt-seconds of the 30 s mean above the budget."""
     p30 = np.asarray(p30, dtype=np.float64)
-    return float(np.sum(np.maximum(0.0, p30 - budget_w)) * dt)
+    return math.fsum(np.maximum(0.0, p30 - budget_w)) * dt
 
 
 def state_vector(p, dt: float, budget_w: float, level: int, prev_level: int, prev_duration_s: float) -> np.ndarray:

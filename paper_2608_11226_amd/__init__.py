@@ -26,6 +26,11 @@ EXPORTED = (
     "grpo_advantages", "rollout_generate", "rollout_sync", "rollout_destroy", "rollout_last_error",
     "rollout_export_weight", "rollout_profile_decode_step",
 )
+# include/occupancy.h: power metrics and threshold policy of the occupancy controller (host code)
+EXPORTED_OCC = (
+    "occ_rolling_mean", "occ_violation", "occ_normalize_budget", "occ_hysteresis_step", "occ_monitor_create",
+    "occ_monitor_push", "occ_monitor_read", "occ_monitor_state", "occ_monitor_destroy",
+)
 
 
 class RolloutError(RuntimeError):
@@ -54,6 +59,14 @@ class Plan(ctypes.Structure):
     ]
 
 
+class OccReading(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int64), ("p_now_w", ctypes.c_double), ("p_5s_ago_w", ctypes.c_double),
+        ("p10_w", ctypes.c_double), ("p30_w", ctypes.c_double), ("violation_rate", ctypes.c_double),
+        ("excess_ws", ctypes.c_double), ("peak30_w", ctypes.c_double),
+    ]
+
+
 class StepProfile(ctypes.Structure):
     _fields_ = [
         ("ms", ctypes.c_double * 3), ("launches", ctypes.c_int32 * 3),
@@ -70,7 +83,7 @@ def _load():
     import torch  # noqa: F401
 
     lib = ctypes.CDLL(LIB_PATH)
-    vp, i32, f32, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_uint64
+    vp, i32, f32, u64, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_uint64, ctypes.c_double
     sig = {
         "rollout_plan": ([ctypes.POINTER(ModelConfig), i32, ctypes.POINTER(Plan)], i32),
         "rollout_init": ([ctypes.POINTER(ModelConfig), vp, u64, vp, ctypes.POINTER(vp)], i32),
@@ -84,6 +97,15 @@ def _load():
         "rollout_last_error": ([vp], ctypes.c_char_p),
         "rollout_export_weight": ([vp, i32, vp], i32),
         "rollout_profile_decode_step": ([vp, vp, vp, ctypes.POINTER(StepProfile)], i32),
+        "occ_rolling_mean": ([vp, ctypes.c_int64, f64, f64, vp], i32),
+        "occ_violation": ([vp, ctypes.c_int64, f64, f64, ctypes.POINTER(f64), ctypes.POINTER(f64)], i32),
+        "occ_normalize_budget": ([f64, f64, f64], f64),
+        "occ_hysteresis_step": ([i32, i32, f64, f64, f64, f64, f64], i32),
+        "occ_monitor_create": ([f64, f64], vp),
+        "occ_monitor_push": ([vp, f64], i32),
+        "occ_monitor_read": ([vp, ctypes.POINTER(OccReading)], i32),
+        "occ_monitor_state": ([vp, i32, i32, f64, vp], i32),
+        "occ_monitor_destroy": ([vp], None),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -180,6 +202,76 @@ SHAPES = {
     "14b": (48, 5120, 40, 8, 128, 13824, 152064, 1e6),
     "72b": (80, 8192, 64, 8, 128, 29568, 152064, 1e6),
 }
+
+
+# ---------------------------------------------------------------------------
+# include/occupancy.h (host code: arrays are float64 NumPy arrays)
+# ---------------------------------------------------------------------------
+def _f64(a):
+    import numpy as np
+
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def occ_rolling_mean(p, dt_s: float, window_s: float):
+    import numpy as np
+
+    p = _f64(p)
+    out = np.empty_like(p)
+    _check(lib.occ_rolling_mean(p.ctypes.data, len(p), dt_s, window_s, out.ctypes.data))
+    return out
+
+
+def occ_violation(p30, budget_w: float, dt_s: float):
+    p30 = _f64(p30)
+    rate, excess = ctypes.c_double(), ctypes.c_double()
+    _check(lib.occ_violation(p30.ctypes.data, len(p30), budget_w, dt_s, ctypes.byref(rate), ctypes.byref(excess)))
+    return rate.value, excess.value
+
+
+def occ_normalize_budget(budget_cal_w: float, p4_new_w: float, p4_cal_w: float) -> float:
+    return lib.occ_normalize_budget(budget_cal_w, p4_new_w, p4_cal_w)
+
+
+def occ_hysteresis_step(level_idx: int, n_levels: int, p30_w: float, p10_w: float, drop_w: float, climb30_w: float,
+                        climb10_w: float) -> int:
+    r = lib.occ_hysteresis_step(level_idx, n_levels, p30_w, p10_w, drop_w, climb30_w, climb10_w)
+    if r < 0:
+        raise RolloutError(EINVAL, "level index outside [0, n_levels)")
+    return r
+
+
+class OccMonitor:
+    """occ_monitor_*: eq. (1) means and eqs. (2)-(3) accumulated over pushed power samples."""
+
+    def __init__(self, dt_s: float, budget_w: float):
+        self.h = lib.occ_monitor_create(dt_s, budget_w)
+        if not self.h:
+            raise RolloutError(EINVAL, "occ_monitor_create: dt_s must be > 0")
+        self.dt_s, self.budget_w = dt_s, budget_w
+
+    def push(self, power_w: float):
+        _check(lib.occ_monitor_push(self.h, power_w))
+
+    def read(self) -> OccReading:
+        r = OccReading()
+        _check(lib.occ_monitor_read(self.h, ctypes.byref(r)))
+        return r
+
+    def state(self, level: int, prev_level: int, prev_duration_s: float):
+        import numpy as np
+
+        out = np.empty(8, dtype=np.float64)
+        _check(lib.occ_monitor_state(self.h, level, prev_level, prev_duration_s, out.ctypes.data))
+        return out
+
+    def close(self):
+        if self.h:
+            lib.occ_monitor_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        self.close()
 
 
 def model_config(shape, dtype: int, max_prompt_len: int, max_new_tokens: int, max_seqs_in_flight: int,

@@ -2,7 +2,8 @@
 
     python -m paper_2608_11226_amd.build [--jobs N]
 
-Every .hip file under csrc/ is compiled with hipcc for gfx950 only and linked
+Every .hip file under csrc/ is compiled with hipcc for gfx950 only, every .cpp
+file there (host code) with the same compiler as plain C++, and all are linked
 into paper_2608_11226_amd/librollout.so.  Packed-fp32 instructions are turned
 off for the device code (the host pass warns that it does not know the
 feature; that is harmless).
@@ -58,7 +59,7 @@ def build(jobs: int | None = None, verbose: bool = True) -> str:
     if not shutil.which(HIPCC) and not os.path.exists(HIPCC):
         raise RuntimeError("hipcc not found; the HIP library cannot be built")
     os.makedirs(BUILD, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
     jobs = jobs or min(16, os.cpu_count() or 1)
     with ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(_compile, srcs))

@@ -10,19 +10,26 @@ import paper_2608_11226_amd as R
 from conftest import ROOT
 
 
-def _declared():
-    src = open(os.path.join(ROOT, "include", "rollout.h")).read()
+def _declared(header, pattern):
+    src = open(os.path.join(ROOT, "include", header)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(rollout_\w+|grpo_\w+)\s*\(", src)))
+    return sorted(set(re.findall(pattern + r"\s*\(", src)))
 
 
 def test_every_declared_symbol_is_exported():
-    names = _declared()
+    names = _declared("rollout.h", r"\b(rollout_\w+|grpo_\w+)")
     assert len(names) >= 12
     lib = ctypes.CDLL(R.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(R.EXPORTED) == names
+    occ = _declared("occupancy.h", r"\b(occ_\w+)")
+    for n in occ:
+        assert hasattr(lib, n), n
+    assert sorted(R.EXPORTED_OCC) == occ
+    # no header under include/ declares a symbol outside these two lists
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == ["occupancy.h", "rollout.h"]
 
 
 def _cfg(shape="7b", dtype=1, P=256, N=512, S=64, budget=288 * 10**9, **kw):
