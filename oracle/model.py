@@ -15,7 +15,7 @@ with these readings where the paper is silent:
 * SwiGLU MLP: down(silu(gate x) * up x), silu(z) = z / (1 + exp(-z)).
 * No biases, untied LM head, logits from the final position(s).
 
-Two numeric modes:
+Three numeric modes:
 
 * ``"fp32"``: weights as generated (fp32 values), everything else float64.
 * ``"bf16"``: the bf16 precision contract.  Values are rounded to bf16
@@ -24,6 +24,9 @@ Two numeric modes:
   output before Wo, silu(g)*u before Wdown, the final-norm output before the
   LM head); q after RoPE; k and v as stored in the cache.  The residual
   stream, accumulations, scores, softmax and logits are not rounded.
+* ``"int4"``: the bf16 contract with the layer projections (q, k, v, o, gate,
+  up, down) stored as int4 codes in groups of 128 (``oracle.quant``); their
+  dequantised values are rounded to bf16.  Embedding and LM head as in bf16.
 
 Parity: ``forward_full`` (no cache, full O(T^2) recompute) and the cached
 ``prefill``/``decode`` path are two independent routes to the same logits and
@@ -113,24 +116,30 @@ class OracleModel:
 
     def __init__(self, shape: workload.ModelShape, weights: dict | None = None, mode: str = "fp32",
                  seed: int = 0, std: float = 0.02):
-        if mode not in ("fp32", "bf16"):
-            raise ValueError("mode must be 'fp32' or 'bf16'")
+        if mode not in ("fp32", "bf16", "int4"):
+            raise ValueError("mode must be 'fp32', 'bf16' or 'int4'")
         self.shape = shape
         self.mode = mode
         if weights is None:
             weights = workload.model_weights(shape, seed=seed, std=std)
-        cast = bf16_round if mode == "bf16" else (lambda a: np.asarray(a, dtype=F64))
+        cast = bf16_round if mode in ("bf16", "int4") else (lambda a: np.asarray(a, dtype=F64))
+        if mode == "int4":
+            from .quant import dequantize_int4, quantize_int4
+
+            cast_layer = lambda a: bf16_round(dequantize_int4(*quantize_int4(a)))
+        else:
+            cast_layer = cast
         self.embed = cast(weights["embed"])
         self.lm_head = cast(weights["lm_head"])
         self.final_norm = np.asarray(weights["final_norm"], dtype=F64)
         self.layers = []
         for l in range(shape.n_layers):
             lw = weights["layers"][l]
-            self.layers.append({k: (np.asarray(v, F64) if k.endswith("norm") else cast(v)) for k, v in lw.items()})
+            self.layers.append({k: (np.asarray(v, F64) if k.endswith("norm") else cast_layer(v)) for k, v in lw.items()})
 
     # rounding at the contract's points (identity in fp32 mode)
     def _r(self, x: np.ndarray) -> np.ndarray:
-        return bf16_round(x) if self.mode == "bf16" else x
+        return bf16_round(x) if self.mode != "fp32" else x
 
     @property
     def n_rep(self) -> int:
