@@ -44,6 +44,12 @@ typedef int32_t rollout_status;
 
 #define ROLLOUT_DTYPE_FP32 0     /* fp32 weights, cache and activations */
 #define ROLLOUT_DTYPE_BF16 1     /* bf16 weights/cache/GEMM operands, fp32 residual and logits */
+#define ROLLOUT_DTYPE_INT4 2     /* as BF16, but the layer projections (q, k, v, o, gate, up, down) are
+                                    weight-only int4: groups of 128 inputs of one output row, each with an
+                                    fp32 scale s and zero point z, w = bf16((q - z) * s) (the AWQ storage
+                                    format of the 72B generation proxy, sections 5 and 6.6); embedding and
+                                    LM head stay bf16.  Needs d_model, n_heads*head_dim and d_ff to be
+                                    multiples of 128. */
 
 typedef struct rollout_ctx rollout_ctx;
 

@@ -25,8 +25,9 @@ Three numeric modes:
   LM head); q after RoPE; k and v as stored in the cache.  The residual
   stream, accumulations, scores, softmax and logits are not rounded.
 * ``"int4"``: the bf16 contract with the layer projections (q, k, v, o, gate,
-  up, down) stored as int4 codes in groups of 128 (``oracle.quant``); their
-  dequantised values are rounded to bf16.  Embedding and LM head as in bf16.
+  up, down) stored as int4 codes in groups of 128 (``oracle.quant``); they
+  multiply with their exact dequantised values (q - z) * s.  Embedding and LM
+  head as in bf16.
 
 Parity: ``forward_full`` (no cache, full O(T^2) recompute) and the cached
 ``prefill``/``decode`` path are two independent routes to the same logits and
@@ -124,9 +125,9 @@ class OracleModel:
             weights = workload.model_weights(shape, seed=seed, std=std)
         cast = bf16_round if mode in ("bf16", "int4") else (lambda a: np.asarray(a, dtype=F64))
         if mode == "int4":
-            from .quant import dequantize_int4, quantize_int4
+            from .quant import dequantize_int4_exact, quantize_int4
 
-            cast_layer = lambda a: bf16_round(dequantize_int4(*quantize_int4(a)))
+            cast_layer = lambda a: dequantize_int4_exact(*quantize_int4(a))
         else:
             cast_layer = cast
         self.embed = cast(weights["embed"])

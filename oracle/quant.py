@@ -14,7 +14,12 @@ Per group of one row (fp32 arithmetic throughout, round-half-even):
     s = (hi - lo) / 15                   (a constant group: s = |hi|, or 1 when it is 0; then w' = w)
     z = clamp(rint(-lo / s), 0, 15)
     q = clamp(rint(w / s) + z, 0, 15)    (the 4-bit code)
-    w' = (q - z) * s                     (the dequantised weight; the model rounds it to bf16)
+    w' = (q - z) * s                     (the dequantised weight)
+
+Reading of the dequantised weight: the model multiplies with w' = (q - z) * s exactly, never rounded to
+bf16 (a group-quantised GEMM applies s to each group's integer dot product; the product of a 4-bit
+integer and an fp32 scale is exact in float64).  ``dequantize_int4`` returns it rounded once to fp32,
+the form a device exports.
 
 Parity: pinned in tests/test_oracle_quant.py by the reconstruction bound |w - w'| <= s, monotonicity of
 the codes, at most 16 distinct values per group, exact reconstruction of 16-level groups, and the
@@ -45,9 +50,18 @@ def quantize_int4(w):
 
 
 def dequantize_int4(q, s, z):
-    """fp32 dequantised weights (q - z) * s."""
+    """fp32 dequantised weights (q - z) * s (the product rounded once to fp32)."""
     q = np.asarray(q, dtype=F32)
     rows, cols = q.shape
     g = q.reshape(rows, cols // GROUP, GROUP)
     out = (g - np.asarray(z, dtype=F32)[:, :, None]) * np.asarray(s, dtype=F32)[:, :, None]
     return out.astype(F32).reshape(rows, cols)
+
+
+def dequantize_int4_exact(q, s, z):
+    """float64 dequantised weights (q - z) * s, exact."""
+    q = np.asarray(q, dtype=np.float64)
+    rows, cols = q.shape
+    g = q.reshape(rows, cols // GROUP, GROUP)
+    out = (g - np.asarray(z, dtype=np.float64)[:, :, None]) * np.asarray(s, dtype=np.float64)[:, :, None]
+    return out.reshape(rows, cols)

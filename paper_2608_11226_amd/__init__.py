@@ -18,7 +18,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "librollout.so")
 
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
-DTYPE_FP32, DTYPE_BF16 = 0, 1
+DTYPE_FP32, DTYPE_BF16, DTYPE_INT4 = 0, 1, 2
 _NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", EDEVICE: "EDEVICE", ESTATE: "ESTATE", EUNSUPPORTED: "EUNSUPPORTED"}
 
 EXPORTED = (

@@ -37,6 +37,15 @@
 // XCD, so its weight tile is fetched into that XCD's L2 once.  The inner loop
 // is bound by LDS bandwidth (fragment reads plus the loads' LDS writes).
 //
+// k_gemm_q4 (decode with int4 layer weights, M <= 64): weights as 4-bit codes
+// in groups of 128 inputs with an fp32 scale and a zero point per row and
+// group; the group's scale multiplies its integer dot product in fp32, so the
+// weights are never rounded.  The codes enter the MFMA as exact bf16 integers
+// (128 + q); a workgroup of four waves shares each group's activation
+// fragments and their sums through LDS.  Larger batches with int4 weights
+// dequantise a projection into two bf16 tile matrices (hi + lo) and take the
+// tile kernel twice.
+//
 // fp32 path: a plain LDS-tiled VALU GEMM over row-major X and W (the fp32
 // path exists for exact parity on small models, not for speed).
 #include <algorithm>
@@ -49,6 +58,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
@@ -238,6 +248,163 @@ __global__ __launch_bounds__(64) void k_gemm_ring(const bf16x8_t* __restrict__ X
   }
 }
 
+// int4 weights (format in synth.hip: codes [N/16][K/128][64][4 words] in AWQ nibble order, then fp32
+// scales and uint8 zeros [N/16][K/128][16]), scaled per group: for a 128-input group g of row n,
+//   y[m] += s[n,g] * sum_k (q[n,k] - z[n,g]) x[m,k].
+// A code q enters the MFMA as the exact bf16 integer 128 + q (the nibble in the mantissa of 128: one
+// shift and one and-or per pair of codes), so a group's MFMA partial is P = sum_k (128 + q) x.  One
+// all-ones MFMA per group gives X = sum_k x[m,k], shared by the wave's weight blocks, and the group's
+// epilogue adds s * (P - (128 + z) * X) to the fp32 accumulator.  The weights are never rounded.
+// Ring over groups as in k_gemm_ring: per group and weight block one 16-byte code load, a 16-byte load
+// of the four scales of the lane's accumulator rows and a 4-byte load of their zeros.
+__device__ __forceinline__ bf16x8_t q4_operand(uint32_t w) {
+  u32x4_t d;
+  d[0] = (w & 0x000F000Fu) | 0x43004300u;
+  d[1] = ((w >> 4) & 0x000F000Fu) | 0x43004300u;
+  d[2] = ((w >> 8) & 0x000F000Fu) | 0x43004300u;
+  d[3] = ((w >> 12) & 0x000F000Fu) | 0x43004300u;
+  return __builtin_bit_cast(bf16x8_t, d);
+}
+
+// A workgroup of four waves shares the activation fragments of a group through LDS (double
+// buffered: wave w loads k-step w of group i + 1 for every 16-row block while all compute group i,
+// then stores it).  Wave w also forms that k-step's activation sums with MB all-ones MFMAs and
+// publishes them; a group's sums X are the four waves' partials added in k-step order.  Each wave
+// owns NBW weight blocks and keeps their codes, scales and zeros in a two-group register ring.
+// One barrier per group.
+template <int MB, int NBW, bool SWI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_gemm_q4(
+    const bf16x8_t* __restrict__ XF, const u32x4_t* __restrict__ Wq, const floatx4_t* __restrict__ Ws,
+    const uint32_t* __restrict__ Wz, float* __restrict__ out, int M, int N, int K, int kslice,
+    uint16_t* __restrict__ h) {
+  constexpr int D = 2;
+  __shared__ bf16x8_t xl[2][4 * MB][64];
+  __shared__ float xsl[2][4][MB][16];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nb0 = (blockIdx.x * 4 + wave) * NBW;
+  const int nbt = N >> 4, gbt = K >> 7;
+  const int kg0 = (int)blockIdx.y * (kslice >> 7);
+  const int ng = min(gbt, kg0 + (kslice >> 7)) - kg0;
+  if (ng <= 0) {  // an empty K split contributes zeros
+    if constexpr (!SWI) {
+      for (int j = 0; j < NBW && nb0 + j < nbt; ++j)
+        for (int m = lane & 15; m < M; m += 16)
+          *reinterpret_cast<float4*>(out + ((size_t)blockIdx.y * M + m) * N + (nb0 + j) * 16 + 4 * (lane >> 4)) =
+              make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    return;
+  }
+  bf16x8_t ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = __builtin_bit_cast(__bf16, (uint16_t)0x3F80);
+  floatx4_t acc[NBW][MB];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  {
+    // wave-uniform bases of each block's first group (blocks past N: clamped, never stored)
+    size_t item0[NBW];
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) item0[j] = (size_t)min(nb0 + j, nbt - 1) * gbt + kg0;
+    const int wl = lane, sl = lane >> 4;
+    // k-step `wave` of a group, every 16-row block: fragments wave * MB .. + MB - 1 of the group's 4 MB
+    const bf16x8_t* xp = XF + (size_t)kg0 * 4 * MB * 64 + (size_t)wave * MB * 64;
+    u32x4_t cr[D][NBW];
+    floatx4_t sr[D][NBW];
+    uint32_t zr[D][NBW];
+    auto load_w = [&](int d, int gg) {
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+        const size_t it = item0[j] + (size_t)gg;
+        cr[d][j] = __builtin_nontemporal_load(Wq + it * 64 + wl);
+        sr[d][j] = Ws[it * 4 + sl];  // scales of rows 4 (lane / 16) .. + 3
+        zr[d][j] = Wz[it * 4 + sl];
+      }
+    };
+    bf16x8_t xst[MB];
+    auto load_x = [&](int gg) {
+#pragma unroll
+      for (int f = 0; f < MB; ++f) xst[f] = xp[((size_t)gg * 4 * MB + f) * 64 + lane];
+    };
+    auto store_x = [&](int buf) {
+#pragma unroll
+      for (int f = 0; f < MB; ++f) {
+        xl[buf][wave * MB + f][lane] = xst[f];
+        const floatx4_t p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, xst[f], floatx4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+        if (lane < 16) xsl[buf][wave][f][lane] = p[0];
+      }
+    };
+    load_x(0);
+    store_x(0);
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      load_w(d, min(d, ng - 1));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    for (int i = 0; i < ng; i += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int g = i + d;                  // group computed now, from LDS buffer g & 1 and ring slot d
+        load_x(min(g + 1, ng - 1));           // next group's fragments (clamped past the end, never used)
+        if (g < ng) {
+          const int buf = g & 1;
+          float xs[MB];
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const int m16 = lane & 15;
+            xs[mb] = ((xsl[buf][0][mb][m16] + xsl[buf][1][mb][m16]) + xsl[buf][2][mb][m16]) + xsl[buf][3][mb][m16];
+          }
+#pragma unroll
+          for (int j = 0; j < NBW; ++j) {
+            floatx4_t pp[MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) pp[mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const bf16x8_t a = q4_operand(cr[d][j][t]);
+#pragma unroll
+              for (int mb = 0; mb < MB; ++mb)
+                pp[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, xl[buf][t * MB + mb][lane], pp[mb], 0, 0, 0);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float sc = sr[d][j][r];
+              const float off = __uint_as_float(0x43000000u | (((zr[d][j] >> (8 * r)) & 0xFFu) << 16));  // 128 + z
+#pragma unroll
+              for (int mb = 0; mb < MB; ++mb) acc[j][mb][r] = fmaf(sc, fmaf(-off, xs[mb], pp[mb][r]), acc[j][mb][r]);
+            }
+          }
+        }
+        load_w(d, min(g + D, ng - 1));
+        store_x((g + 1) & 1);  // buffer (g + 1) & 1 was last read for group g - 1, before the last barrier
+        __syncthreads();
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    if (nb0 + j >= nbt) continue;
+    const int n = (nb0 + j) * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = mb * 16 + (lane & 15);
+      if (m >= M) continue;
+      if constexpr (SWI) {
+        const float g0 = acc[j][mb][0], u0 = acc[j][mb][1], g1 = acc[j][mb][2], u1 = acc[j][mb][3];
+        const float h0 = g0 / (1.0f + expf(-g0)) * u0, h1 = g1 / (1.0f + expf(-g1)) * u1;
+        *reinterpret_cast<uint32_t*>(h + xoff(h, m, n >> 1, N >> 1, MB)) = pack_bf16x2(h0, h1);
+      } else {
+        float* o = out + (size_t)blockIdx.y * M * N;
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) =
+            make_float4(acc[j][mb][0], acc[j][mb][1], acc[j][mb][2], acc[j][mb][3]);
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, int ldx, const float* __restrict__ W,
                                                   float* __restrict__ out, int M, int N, int K) {
   __shared__ float xs[16][33];
@@ -259,11 +426,6 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   }
   const int m = m0 + ty, n = n0 + tx;
   if (m < M && n < N) out[(size_t)m * N + n] = acc;
-}
-
-int env_int(const char* name, int dflt) {
-  const char* v = std::getenv(name);
-  return v ? std::atoi(v) : dflt;
 }
 
 int kslice_for(int K, int splits) {
@@ -311,7 +473,64 @@ hipError_t launch_ring(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, floa
   return hipGetLastError();
 }
 
+// int4 ring: K slices in whole 128-wide groups
+int kslice_q4(int K, int splits) {
+  const int per = (K + splits - 1) / splits;
+  return (per + 127) / 128 * 128;
+}
+
+template <int MB, int NBW, bool SWI>
+void launch_q4_mb(hipStream_t s, const bf16x8_t* x, const void* w, float* out, int M, int N, int K, int splits,
+                  uint16_t* h) {
+  const int kslice = kslice_q4(K, splits);
+  const dim3 grid((N / 16 + 4 * NBW - 1) / (4 * NBW), splits);
+  const char* base = (const char*)w;
+  const u32x4_t* wq = (const u32x4_t*)base;
+  const floatx4_t* ws = (const floatx4_t*)(base + q4_code_bytes(N, K));
+  const uint32_t* wz = (const uint32_t*)(base + q4_code_bytes(N, K) + (size_t)N * (K / 128) * 4);
+  hipLaunchKernelGGL((k_gemm_q4<MB, NBW, SWI>), grid, dim3(256), 0, s, x, wq, ws, wz, out, M, N, K, kslice, h);
+}
+
+// Weight blocks per wave: 4 for up to two 16-row activation blocks, 2 above (registers: both fit two
+// waves per SIMD).  K splits aim at 512 workgroups, two per CU.
+constexpr int q4_blocks(int M) { return M <= 32 ? 4 : 2; }
+constexpr int kQ4TargetWorkgroups = 512;
+
+template <bool SWI>
+hipError_t launch_q4(hipStream_t s, const bf16x8_t* x, const void* w, float* out, int M, int N, int K, int splits,
+                     uint16_t* h) {
+  switch ((M + 15) / 16) {
+    case 1: launch_q4_mb<1, q4_blocks(16), SWI>(s, x, w, out, M, N, K, splits, h); break;
+    case 2: launch_q4_mb<2, q4_blocks(32), SWI>(s, x, w, out, M, N, K, splits, h); break;
+    case 3: launch_q4_mb<3, q4_blocks(48), SWI>(s, x, w, out, M, N, K, splits, h); break;
+    default: launch_q4_mb<4, q4_blocks(64), SWI>(s, x, w, out, M, N, K, splits, h); break;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
+
+int gemm_splits_q4(int M, int N, int K, int max_splits) {
+  if (M > kRingMaxRows || max_splits <= 1) return 1;
+  const int groups = (N / 16 + 4 * q4_blocks(M) - 1) / (4 * q4_blocks(M));  // workgroups per K split
+  int s = (kQ4TargetWorkgroups + groups - 1) / groups;
+  s = std::min(s, std::max(1, K / 256));
+  s = std::max(1, std::min(s, max_splits));
+  const int ks = kslice_q4(K, s);
+  return (K + ks - 1) / ks;
+}
+
+hipError_t launch_gemm_q4(hipStream_t s, const void* X, const void* W, float* out, int M, int N, int K, int splits) {
+  if (M <= 0) return hipSuccess;
+  if (M > kRingMaxRows || N % 16 || K % 128 || splits < 1) return hipErrorInvalidValue;
+  return launch_q4<false>(s, (const bf16x8_t*)X, W, out, M, N, K, splits, nullptr);
+}
+
+hipError_t launch_gemm_swiglu_q4(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h) {
+  if (M <= 0) return hipSuccess;
+  if (M > kSwigluMaxRows || M > kRingMaxRows || N % 16 || K % 128) return hipErrorInvalidValue;
+  return launch_q4<true>(s, (const bf16x8_t*)X, W, nullptr, M, N, K, 1, (uint16_t*)h);
+}
 
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;

@@ -17,7 +17,8 @@ struct Dims {
   int L, d, nh, nkv, hd, ff, V;
   int qd, kvd, nqkv;  // nh*hd, nkv*hd, qd + 2*kvd
   float eps, theta;
-  int dtype;          // ROLLOUT_DTYPE_*
+  int dtype;          // ROLLOUT_DTYPE_FP32 or _BF16: activations, cache, embedding and LM head
+  bool wq4;           // layer projections stored as int4 groups (ROLLOUT_DTYPE_INT4; dtype is then BF16)
   int blk;            // tokens per KV block
   int max_ctx;        // max prompt + max new tokens
 };
@@ -62,6 +63,15 @@ struct RowMap {
 // ---------------------------------------------------------------------------
 hipError_t launch_synth(hipStream_t s, void* dst, int dtype, const WeightDesc& w, uint64_t seed, double std_);
 hipError_t launch_fill(hipStream_t s, float* dst, size_t n, float value);
+// int4 weight-only matrices (layer projections of the int4 model): packed codes, then fp32 scales,
+// then uint8 zero points, q4_code_bytes + q4_sz_bytes in all; rows a multiple of 16, cols of 128.
+// The code, scale and zero arrays start at byte offsets 0, rows*cols/2 and rows*cols/2 + 4*rows*cols/128.
+size_t q4_code_bytes(int rows, int cols);
+size_t q4_sz_bytes(int rows, int cols);
+hipError_t launch_synth_q4(hipStream_t s, void* dst, const WeightDesc& w, uint64_t seed, double std_);
+hipError_t launch_export_q4(hipStream_t s, const void* src, const WeightDesc& w, int which, int rows, float* out);
+// bf16 MFMA-operand tiles hi = bf16(w), lo = bf16(w - hi) of an int4 matrix (each rows * cols bf16)
+hipError_t launch_dequant_q4(hipStream_t s, const void* src, int rows, int cols, void* dst_hi, void* dst_lo);
 hipError_t launch_export(hipStream_t s, const void* src, int dtype, const WeightDesc& w, int which, int rows,
                          float* out);
 
@@ -75,6 +85,10 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
 // row i at 2i + 1; h[m][i] = silu(gate) * up in the down projection's operand layout.
 constexpr int kSwigluMaxRows = 64;
 hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h);
+// The same two GEMMs over an int4 weight matrix (M <= 64; K a multiple of 128; partial splits as above).
+int gemm_splits_q4(int M, int N, int K, int max_splits);
+hipError_t launch_gemm_q4(hipStream_t s, const void* X, const void* W, float* out, int M, int N, int K, int splits);
+hipError_t launch_gemm_swiglu_q4(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h);
 
 hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
                         const int32_t* col, int M, int d, int V, float* x, int32_t* err);

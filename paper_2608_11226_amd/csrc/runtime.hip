@@ -41,7 +41,7 @@ struct Layout {
   size_t rope_cos = 0, rope_sin = 0;
   size_t weights_end = 0;  // weights + rope tables
   size_t x = 0, a = 0, q = 0, o = 0, h = 0, a_last = 0, part = 0, opart = 0, ml = 0, logits = 0;
-  size_t tables = 0, ctx_len = 0, cols = 0, err = 0, samp = 0;
+  size_t tables = 0, ctx_len = 0, cols = 0, err = 0, samp = 0, wdq = 0;
   size_t work_end = 0;     // start of the KV pool
   size_t weight_bytes = 0, work_bytes = 0, kv_block_bytes = 0;
   int S = 0, R = 0, T_chunk = 0, max_blocks = 0, attn_splits_max = 1;
@@ -62,7 +62,8 @@ Dims make_dims(const rollout_model_config& c) {
   D.nqkv = D.qd + 2 * D.kvd;
   D.eps = c.rms_eps;
   D.theta = c.rope_theta;
-  D.dtype = c.dtype;
+  D.dtype = c.dtype == ROLLOUT_DTYPE_INT4 ? ROLLOUT_DTYPE_BF16 : c.dtype;
+  D.wq4 = c.dtype == ROLLOUT_DTYPE_INT4;
   D.blk = c.kv_block_size;
   D.max_ctx = c.max_prompt_len + c.max_new_tokens;
   return D;
@@ -76,7 +77,10 @@ rollout_status validate_config(const rollout_model_config* c, std::string* msg) 
     *msg = "model dimensions must be positive (vocab >= 2)";
     return ROLLOUT_EINVAL;
   }
-  if (c->dtype != ROLLOUT_DTYPE_FP32 && c->dtype != ROLLOUT_DTYPE_BF16) { *msg = "dtype must be 0 (fp32) or 1 (bf16)"; return ROLLOUT_EINVAL; }
+  if (c->dtype != ROLLOUT_DTYPE_FP32 && c->dtype != ROLLOUT_DTYPE_BF16 && c->dtype != ROLLOUT_DTYPE_INT4) {
+    *msg = "dtype must be 0 (fp32), 1 (bf16) or 2 (int4 layer weights)";
+    return ROLLOUT_EINVAL;
+  }
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f) || !(c->weight_std > 0.0)) {
     *msg = "rms_eps > 0, rope_theta > 1 and weight_std > 0 are required";
     return ROLLOUT_EINVAL;
@@ -92,6 +96,10 @@ rollout_status validate_config(const rollout_model_config* c, std::string* msg) 
   }
   if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32 || c->d_ff % 32 || c->vocab % 16) {
     *msg = "d_model, n_heads*head_dim and d_ff must be multiples of 32, vocab a multiple of 16";
+    return ROLLOUT_EUNSUPPORTED;
+  }
+  if (c->dtype == ROLLOUT_DTYPE_INT4 && (c->d_model % 128 || (c->n_heads * c->head_dim) % 128 || c->d_ff % 128)) {
+    *msg = "int4 weights need d_model, n_heads*head_dim and d_ff to be multiples of 128 (the quantisation group)";
     return ROLLOUT_EUNSUPPORTED;
   }
   if (c->kv_block_size != 8 && c->kv_block_size != 16 && c->kv_block_size != 32) {
@@ -119,7 +127,9 @@ size_t max_part_elems(const Dims& D, int R) {
   const int Ks[4] = {D.d, D.qd, D.d, D.ff};
   for (int M = 1; M <= R; ++M)
     for (int j = 0; j < 4; ++j) {
-      const int s = gemm_splits(D.dtype, M, Ns[j], Ks[j], kMaxSplits);
+      int s = gemm_splits(D.dtype, M, Ns[j], Ks[j], kMaxSplits);
+      if (D.wq4)  // int4: the ring's splits, or two bf16 GEMMs (hi and lo) of up to half the splits each
+        s = std::max(gemm_splits_q4(M, Ns[j], Ks[j], kMaxSplits), 2 * gemm_splits(D.dtype, M, Ns[j], Ks[j], kMaxSplits / 2));
       best = std::max(best, (size_t)s * (size_t)M * (size_t)Ns[j]);
     }
   return best;
@@ -135,14 +145,18 @@ Layout make_layout(const Dims& D, int S, int max_prompt_len) {
     off = align_up(off + bytes);
     return o;
   };
+  // a layer projection of N outputs over K inputs
+  auto proj_bytes = [&](int N, int K) {
+    return D.wq4 ? q4_code_bytes(N, K) + q4_sz_bytes(N, K) : (size_t)N * K * eb;
+  };
   Lo.embed = take((size_t)D.V * D.d * eb);
   Lo.layers.resize(D.L);
   for (int l = 0; l < D.L; ++l) {
     Layer& y = Lo.layers[l];
-    y.wqkv = take((size_t)D.nqkv * D.d * eb);
-    y.wo = take((size_t)D.d * D.qd * eb);
-    y.wgu = take((size_t)2 * D.ff * D.d * eb);
-    y.wdown = take((size_t)D.d * D.ff * eb);
+    y.wqkv = take(proj_bytes(D.nqkv, D.d));
+    y.wo = take(proj_bytes(D.d, D.qd));
+    y.wgu = take(proj_bytes(2 * D.ff, D.d));
+    y.wdown = take(proj_bytes(D.d, D.ff));
     y.attn_norm = take((size_t)D.d * 4);
     y.mlp_norm = take((size_t)D.d * 4);
   }
@@ -177,6 +191,9 @@ Layout make_layout(const Dims& D, int S, int max_prompt_len) {
   Lo.ctx_len = Lo.tables + (size_t)S * Lo.max_blocks * 4;
   Lo.cols = take(64);
   Lo.err = take(64);
+  // int4: batches above the ring GEMM's rows multiply bf16 hi and lo copies of one projection at a time
+  if (D.wq4)
+    Lo.wdq = take(std::max(std::max((size_t)D.nqkv * D.d, (size_t)D.d * D.qd), (size_t)2 * D.ff * D.d) * 4);
   Lo.work_end = off;
   Lo.work_bytes = Lo.work_end - Lo.weights_end;
   Lo.kv_block_bytes = (size_t)D.L * D.nkv * 2 * D.blk * D.hd * eb;
@@ -295,11 +312,44 @@ rollout_status gemm(rollout_ctx* c, const void* X, const void* W, float* out, in
   return ROLLOUT_OK;
 }
 
-// Decode gate/up GEMM with SwiGLU applied to its own output (bf16, M <= kSwigluMaxRows).
+// Decode gate/up GEMM with SwiGLU applied to its own output (bf16 or int4 weights, M <= kSwigluMaxRows).
 rollout_status gemm_swiglu(rollout_ctx* c, const void* X, const void* W, int M, int N, int K, void* h) {
   const double eb = (double)elem_bytes(c->D.dtype);
-  Scope sc(c, 0, (double)N * K * eb + (double)M * K * eb + (double)M * (N / 2) * eb, 2.0 * M * N * K);
-  HIP_TRY(c, launch_gemm_swiglu(c->stream, X, W, M, N, K, h), "gemm");
+  const double wb = c->D.wq4 ? (double)(q4_code_bytes(N, K) + q4_sz_bytes(N, K)) : (double)N * K * eb;
+  Scope sc(c, 0, wb + (double)M * K * eb + (double)M * (N / 2) * eb, 2.0 * M * N * K);
+  if (c->D.wq4)
+    HIP_TRY(c, launch_gemm_swiglu_q4(c->stream, X, W, M, N, K, h), "gemm");
+  else
+    HIP_TRY(c, launch_gemm_swiglu(c->stream, X, W, M, N, K, h), "gemm");
+  return ROLLOUT_OK;
+}
+
+// A layer projection.  int4 matrices take the int4 ring GEMM for decode batches; larger batches
+// (prefill) dequantise the matrix into bf16 tiles first and take the bf16 GEMM.
+rollout_status proj(rollout_ctx* c, const void* X, const void* W, float* out, int M, int N, int K, int* splits_out) {
+  if (!c->D.wq4) return gemm(c, X, W, out, M, N, K, kMaxSplits, splits_out);
+  const double wb = (double)(q4_code_bytes(N, K) + q4_sz_bytes(N, K));
+  if (M <= kSwigluMaxRows) {
+    const int s = gemm_splits_q4(M, N, K, kMaxSplits);
+    if ((size_t)s * M * N > c->Lo.part_elems) return fail(c, ROLLOUT_EINVAL, "internal: split-K workspace too small");
+    Scope sc(c, 0, wb + (double)M * K * 2 + (double)s * M * N * 4, 2.0 * M * N * K);
+    HIP_TRY(c, launch_gemm_q4(c->stream, X, W, out, M, N, K, s), "gemm");
+    *splits_out = s;
+    return ROLLOUT_OK;
+  }
+  // w = hi + lo with hi = bf16(w), lo = bf16(w - hi): two bf16 GEMMs into consecutive split slots
+  char* hi = c->at<char>(c->Lo.wdq);
+  char* lo = hi + (size_t)N * K * 2;
+  {
+    Scope sc(c, 2, wb + (double)N * K * 4, 0);
+    HIP_TRY(c, launch_dequant_q4(c->stream, W, N, K, hi, lo), "dequantise");
+  }
+  int s1 = 0, s2 = 0;
+  rollout_status r = gemm(c, X, hi, out, M, N, K, kMaxSplits / 2, &s1);
+  if (r) return r;
+  if ((size_t)2 * s1 * M * N > c->Lo.part_elems) return fail(c, ROLLOUT_EINVAL, "internal: split-K workspace too small");
+  if ((r = gemm(c, X, lo, out + (size_t)s1 * M * N, M, N, K, kMaxSplits / 2, &s2))) return r;
+  *splits_out = s1 + s2;
   return ROLLOUT_OK;
 }
 
@@ -344,7 +394,7 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
   for (int l = 0; l < D.L; ++l) {
     const Layer& y = Lo.layers[l];
     int s;
-    rollout_status r = gemm(c, a, c->at(y.wqkv), part, M, D.nqkv, D.d, kMaxSplits, &s);
+    rollout_status r = proj(c, a, c->at(y.wqkv), part, M, D.nqkv, D.d, &s);
     if (r) return r;
     // decode rows: attention rotates q/k and appends k/v itself, straight from the split partials
     const bool attn_qkv = rm.P == 0 && attention_forms_qkv(D);
@@ -365,7 +415,7 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
                                     opart, ml, o, err, attn_qkv ? part : nullptr, s, c->at<float>(Lo.rope_cos),
                                     c->at<float>(Lo.rope_sin)), "attention");
     }
-    r = gemm(c, o, c->at(y.wo), part, M, D.d, D.qd, kMaxSplits, &s);
+    r = proj(c, o, c->at(y.wo), part, M, D.d, D.qd, &s);
     if (r) return r;
     {
       Scope sc(c, 2, (double)s * M * D.d * 4 + (double)M * D.d * (8 + eb), 0);
@@ -375,11 +425,11 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
     if (D.dtype == ROLLOUT_DTYPE_BF16 && M <= kSwigluMaxRows) {
       if ((r = gemm_swiglu(c, a, c->at(y.wgu), M, 2 * D.ff, D.d, h))) return r;
     } else {
-      if ((r = gemm(c, a, c->at(y.wgu), part, M, 2 * D.ff, D.d, kMaxSplits, &s))) return r;
+      if ((r = proj(c, a, c->at(y.wgu), part, M, 2 * D.ff, D.d, &s))) return r;
       Scope sc(c, 2, (double)s * M * 2 * D.ff * 4 + (double)M * D.ff * eb, 0);
       HIP_TRY(c, launch_swiglu(c->stream, D.dtype, part, s, M, D.ff, h), "swiglu");
     }
-    r = gemm(c, h, c->at(y.wdown), part, M, D.d, D.ff, kMaxSplits, &s);
+    r = proj(c, h, c->at(y.wdown), part, M, D.d, D.ff, &s);
     if (r) return r;
     {
       const float* next_gain = l + 1 < D.L ? c->at<float>(Lo.layers[l + 1].attn_norm) : c->at<float>(Lo.final_norm);
@@ -591,10 +641,14 @@ rollout_status rollout_init(const rollout_model_config* cfg, void* d_arena, uint
   for (int l = 0; l < D.L; ++l) {
     const Layer& y = Lo.layers[l];
     const int b = 1 + 9 * l;
-    if ((e = launch_synth(c->stream, c->at(y.wqkv), D.dtype, wdesc(D.nqkv, D.d, lay, FUSE_QKV, b + 1, b + 2, b + 3, D.qd, D.kvd), seed, sd)) ||
-        (e = launch_synth(c->stream, c->at(y.wo), D.dtype, wdesc(D.d, D.qd, lay, FUSE_NONE, b + 4), seed, sd)) ||
-        (e = launch_synth(c->stream, c->at(y.wgu), D.dtype, wdesc(2 * D.ff, D.d, lay, FUSE_GU, b + 6, b + 7), seed, sd)) ||
-        (e = launch_synth(c->stream, c->at(y.wdown), D.dtype, wdesc(D.d, D.ff, lay, FUSE_NONE, b + 8), seed, sd)) ||
+    // layer projections: int4 groups quantised from the same fp32 values, or the dtype's layout
+    auto synth_proj = [&](void* dst, const WeightDesc& w) {
+      return D.wq4 ? launch_synth_q4(c->stream, dst, w, seed, sd) : launch_synth(c->stream, dst, D.dtype, w, seed, sd);
+    };
+    if ((e = synth_proj(c->at(y.wqkv), wdesc(D.nqkv, D.d, lay, FUSE_QKV, b + 1, b + 2, b + 3, D.qd, D.kvd))) ||
+        (e = synth_proj(c->at(y.wo), wdesc(D.d, D.qd, lay, FUSE_NONE, b + 4))) ||
+        (e = synth_proj(c->at(y.wgu), wdesc(2 * D.ff, D.d, lay, FUSE_GU, b + 6, b + 7))) ||
+        (e = synth_proj(c->at(y.wdown), wdesc(D.d, D.ff, lay, FUSE_NONE, b + 8))) ||
         (e = launch_fill(c->stream, c->at<float>(y.attn_norm), D.d, 1.0f)) ||
         (e = launch_fill(c->stream, c->at<float>(y.mlp_norm), D.d, 1.0f)))
       return bad(e, "synth layer");
@@ -791,16 +845,19 @@ rollout_status rollout_export_weight(rollout_ctx* ctx, int32_t tensor_id, float*
   } else if (tensor_id >= 1 && tensor_id < 1 + 9 * D.L) {
     const int l = (tensor_id - 1) / 9, slot = (tensor_id - 1) % 9;
     const Layer& y = Lo.layers[l];
+    // int4 projections export their dequantised (bf16-rounded) values
+    auto exp = [&](const void* src, const WeightDesc& w, int which, int rows) {
+      return D.wq4 ? launch_export_q4(ctx->stream, src, w, which, rows, d_out)
+                   : launch_export(ctx->stream, src, D.dtype, w, which, rows, d_out);
+    };
     switch (slot) {
       case 1: case 2: case 3:
-        e = launch_export(ctx->stream, ctx->at(y.wqkv), D.dtype, wdesc(D.nqkv, D.d, lay, FUSE_QKV, 0, 0, 0, D.qd, D.kvd),
-                          slot - 1, slot == 1 ? D.qd : D.kvd, d_out);
+        e = exp(ctx->at(y.wqkv), wdesc(D.nqkv, D.d, lay, FUSE_QKV, 0, 0, 0, D.qd, D.kvd), slot - 1,
+                slot == 1 ? D.qd : D.kvd);
         break;
-      case 4: e = launch_export(ctx->stream, ctx->at(y.wo), D.dtype, wdesc(D.d, D.qd, lay, FUSE_NONE, 0), 0, D.d, d_out); break;
-      case 6: case 7:
-        e = launch_export(ctx->stream, ctx->at(y.wgu), D.dtype, wdesc(2 * D.ff, D.d, lay, FUSE_GU, 0), slot - 6, D.ff, d_out);
-        break;
-      case 8: e = launch_export(ctx->stream, ctx->at(y.wdown), D.dtype, wdesc(D.d, D.ff, lay, FUSE_NONE, 0), 0, D.d, d_out); break;
+      case 4: e = exp(ctx->at(y.wo), wdesc(D.d, D.qd, lay, FUSE_NONE, 0), 0, D.d); break;
+      case 6: case 7: e = exp(ctx->at(y.wgu), wdesc(2 * D.ff, D.d, lay, FUSE_GU, 0), slot - 6, D.ff); break;
+      case 8: e = exp(ctx->at(y.wdown), wdesc(D.d, D.ff, lay, FUSE_NONE, 0), 0, D.d); break;
       default: return fail(ctx, ROLLOUT_EINVAL, "tensor id names a norm gain, not a matrix");
     }
   } else {

@@ -46,6 +46,23 @@ def test_plan_weight_bytes_match_the_shapes():
         assert 0 <= p.weight_bytes - (2 * matrices + 4 * norms) < 256 * (6 * R.SHAPES[shape][0] + 4)
 
 
+def test_plan_int4_weight_bytes():
+    # int4 layer projections: half a byte per weight plus an fp32 scale and a uint8 zero per 128-input group;
+    # embedding and LM head stay bf16
+    for shape in ("7b", "72b"):
+        L, d, nh, nkv, hd, ff, V, _ = R.SHAPES[shape]
+        proj = (nh * hd + 2 * nkv * hd) * d + d * nh * hd + 2 * ff * d + d * ff
+        want = L * (proj // 2 + proj // 128 * 5) + 2 * V * d * 2 + (2 * L + 1) * d * 4
+        p = R.rollout_plan(_cfg(shape, dtype=R.DTYPE_INT4), 8)
+        assert 0 <= p.weight_bytes - want < 256 * (6 * L + 4)
+        assert p.weight_bytes < 0.4 * R.rollout_plan(_cfg(shape), 8).weight_bytes  # bf16 embedding and head remain
+    # the quantisation group spans 128 inputs: K dimensions must be multiples of 128
+    bad = _cfg((2, 160, 5, 5, 32, 512, 1024, 1e4), dtype=R.DTYPE_INT4, P=16, N=16, S=8)
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_plan(bad, 4)
+    assert e.value.code == R.EUNSUPPORTED and "128" in R.rollout_last_error()
+
+
 def test_plan_kv_blocks_share_prompt_blocks():
     P, N, G, S = 256, 512, 8, 64
     p = R.rollout_plan(_cfg(P=P, N=N, S=S), G)

@@ -47,7 +47,7 @@ def test_bound_monotonicity_and_levels(seed):
             assert q[r, sl].min() <= 1 and q[r, sl].max() >= 14
 
 
-def test_int4_model_rounds_dequantised_layers_only():
+def test_int4_model_uses_exact_dequantised_layers_only():
     shape = W.ModelShape(1, 128, 2, 1, 64, 256, 512)
     wts = W.model_weights(shape)
     m = OracleModel(shape, wts, mode="int4")
@@ -56,5 +56,12 @@ def test_int4_model_rounds_dequantised_layers_only():
     wq = wts["layers"][0]["wq"]
     assert np.array_equal(m.layers[0]["wq"], b.layers[0]["wq"]) is False
     q, s, z = quantize_int4(wq)
+    got = m.layers[0]["wq"]
+    # every weight is a whole number of its group's steps: w' / s = q - z exactly (the product is not rounded)
+    steps = got / np.repeat(s, GROUP, axis=1).astype(np.float64)
+    assert np.array_equal(steps, np.round(steps)) and np.abs(steps).max() <= 15
+    assert np.array_equal(steps, q.astype(np.float64) - np.repeat(z, GROUP, axis=1))
+    # rounded once to fp32 it is the exported form; rounding to bf16 would change some weights
+    assert np.array_equal(got.astype(np.float32), dequantize_int4(q, s, z))
     from oracle.model import bf16_round
-    assert np.array_equal(m.layers[0]["wq"], bf16_round(dequantize_int4(q, s, z)))
+    assert not np.array_equal(got, bf16_round(got))
