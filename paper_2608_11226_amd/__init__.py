@@ -6,7 +6,7 @@ HIP kernels.  The functions below carry the names of the C ABI in
 whose ``data_ptr()`` is passed); PyTorch is used by ``Engine`` only to
 allocate device memory and to provide the stream.
 
-The library must have been built (``python -m paper_2608_11226_amd.build``);
+The library must have been built (``python paper_2608_11226_amd/build.py``);
 importing this package fails loudly when it has not.
 """
 from __future__ import annotations
@@ -76,7 +76,7 @@ class StepProfile(ctypes.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_11226_amd.build`")
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2608_11226_amd/build.py`")
     # torch's libraries link the HIP runtime it ships under an unversioned name;
     # loading torch first lets librollout's libamdhip64.so.7 / libhsa-runtime64.so.1
     # resolve to those same copies, so the process holds one HIP runtime.

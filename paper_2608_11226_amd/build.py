@@ -1,6 +1,8 @@
 """Build librollout.so (HIP for gfx950) in-tree.
 
-    python -m paper_2608_11226_amd.build [--jobs N]
+    python paper_2608_11226_amd/build.py [--jobs N]
+
+(run by path: importing the package needs the library this script builds)
 
 Every .hip file under csrc/ is compiled with hipcc for gfx950 only, every .cpp
 file there (host code) with the same compiler as plain C++, and all are linked
