@@ -25,17 +25,17 @@
 // projection's operand layout.
 //
 // k_gemm_tile (prefill and other batches above 64 rows): a workgroup of four
-// waves owns a 128 x 128 output tile (8 weight blocks x 8 activation blocks,
-// 64 x 64 per wave, 16 MFMAs per k-step from 8 LDS fragment reads).  Both
-// operands reach LDS by direct global-to-LDS loads, one 1 KB fragment per
-// wave instruction (the HBM layouts are already fragment order), into a
-// double buffer of two k-steps per stage; the wave waits for its own loads
-// with an explicit count and a barrier publishes the stage.  The loads are
-// written as inline asm so the compiler neither drains them at the barrier nor
-// orders LDS reads behind them; the explicit wait is what makes the stage
-// visible.  Workgroup order is XCD-aware: the M tiles of one N tile run on one
-// XCD, so its weight tile is fetched into that XCD's L2 once.  The inner loop
-// is bound by LDS bandwidth (fragment reads plus the loads' LDS writes).
+// waves owns 256 weight rows x 128 activation rows; each wave owns its own 64
+// weight rows against all 128 activation rows (4 x 8 MFMA tiles, 128
+// accumulator registers, two waves per SIMD).  The weights never touch LDS:
+// each wave streams its own weight fragments from global memory straight into
+// a three-deep register ring (no two waves read the same weight fragment).
+// The activation fragments are shared by the four waves through a double LDS
+// buffer, staged global -> registers -> LDS three k-steps ahead.  Per k-step
+// a wave reads 8 KB from LDS for 32 MFMAs; one barrier per k-step.  All waits
+// are compiler-placed on loads issued a step or more earlier.  Workgroup order
+// is XCD-aware: the M tiles of one N tile run on one XCD, so its weight tile
+// is fetched into that XCD's L2 once and served to the rest from there.
 //
 // k_gemm_q4 (decode with int4 layer weights, M <= 64): weights as 4-bit codes
 // in groups of 128 inputs with an fp32 scale and a zero point per row and
@@ -64,103 +64,113 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-// s_waitcnt immediate that waits until at most n vector memory operations are outstanding
-constexpr int vm_wait(int n) { return (n & 0xF) | ((n & 0x30) << 10) | (0x7 << 4) | (0xF << 8); }
+// LDS barrier: this wave's LDS writes are complete, then every wave of the workgroup has arrived.  Written
+// as one asm statement with a memory clobber so that no LDS access moves across it and no wait for
+// outstanding global loads (the register prefetch) is added.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// KS k-steps per stage, NS stages in the LDS ring.
-template <int KS, int NS>
-__global__ __launch_bounds__(256) void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
-                                                   float* __restrict__ out, int M, int N, int K, int kslice) {
-  constexpr int FPW = 4 * KS;  // fragments each wave loads per stage (8 KS of W, 8 KS of X per workgroup)
-  __shared__ bf16x8_t lds[NS][2][8][KS][64];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+// Tile kernel: 4 waves, 256 weight rows x 128 activation rows per workgroup, each wave 64 x 128.
+constexpr int kTileNB = 4;            // 16-row weight blocks per wave
+constexpr int kTileMB = 8;            // 16-row activation blocks per workgroup
+constexpr int kTileWaves = 4;
+constexpr int kTileXPW = kTileMB / kTileWaves;  // activation fragments each wave stages per k-step
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W, float* __restrict__ out,
+                 int M, int N, int K, int kslice) {
+  __shared__ bf16x8_t xs[2][kTileMB][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nbt = N >> 4, kbt = K >> 5, Mb = (M + 15) >> 4;
-  const int Mt = (Mb + 7) / 8, Nt = (nbt + 7) / 8;
-  // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD
+  const int Mt = (Mb + kTileMB - 1) / kTileMB, Nt = (nbt + kTileNB * kTileWaves - 1) / (kTileNB * kTileWaves);
+  // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD and its L2
   const int b = blockIdx.x;
   const int grp = b / (8 * Mt), rem = b % (8 * Mt);
   const int nt = grp * 8 + rem % 8, mt = rem / 8;
   if (nt >= Nt) return;
-  const int nb0 = nt * 8, mb0 = mt * 8;
+  const int nb0 = nt * kTileNB * kTileWaves + wave * kTileNB, mb0 = mt * kTileMB;
   const int kb0 = (int)blockIdx.y * (kslice >> 5);
   const int nk = min(kbt, kb0 + (kslice >> 5)) - kb0;
-  const int nst = (nk + KS - 1) / KS;
-  floatx4_t acc[4][4];
+  floatx4_t acc[kTileNB][kTileMB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int j = 0; j < kTileNB; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  if (nst > 0) {
-    // this wave's fragments of a stage: ids wave*FPW .. +FPW-1 over [W|X][block][k-step], clamped into range
-    const bf16x8_t* src[FPW];
-    uint32_t dst[FPW];
-    int fks[FPW];
-    bool fw[FPW];
+    for (int i = 0; i < kTileMB; ++i) acc[j][i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  if (nk > 0) {
+    // every load is unconditional: block and k indices are clamped into range, surplus k-steps are not computed
+    const bf16x8_t* wp[kTileNB];
 #pragma unroll
-    for (int f = 0; f < FPW; ++f) {
-      const int id = wave * FPW + f;
-      const int op = id / (8 * KS), blk = (id % (8 * KS)) / KS;
-      fks[f] = id % KS;
-      fw[f] = op == 0;
-      src[f] = op == 0 ? W + ((size_t)min(nb0 + blk, nbt - 1) * kbt + kb0) * 64 + lane
-                       : XF + ((size_t)kb0 * Mb + min(mb0 + blk, Mb - 1)) * 64 + lane;
-      dst[f] = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)&lds[0][op][blk][fks[f]][0];
-    }
-    constexpr uint32_t kStageBytes = 2 * 8 * KS * 64 * 16;
-    auto issue = [&](int st) {  // stage st (past the end: reloads the last k-step, never computed)
-      const uint32_t base = (uint32_t)(st % NS) * kStageBytes;
+    for (int j = 0; j < kTileNB; ++j) wp[j] = W + ((size_t)min(nb0 + j, nbt - 1) * kbt + kb0) * 64 + lane;
+    const bf16x8_t* xp[kTileXPW];
 #pragma unroll
-      for (int f = 0; f < FPW; ++f) {
-        const int kk = min(st * KS + fks[f], nk - 1);
-        const bf16x8_t* p = src[f] + (size_t)kk * (fw[f] ? 64 : (size_t)Mb * 64);
-        // M0 holds the LDS destination; it is restored, and one wait state separates its write from the load
-        int saved;
-        asm volatile(
-            "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
-            : "=&s"(saved)
-            : "v"(p), "s"(__builtin_amdgcn_readfirstlane(dst[f] + base))
-            : "memory");
-      }
+    for (int i = 0; i < kTileXPW; ++i)
+      xp[i] = XF + ((size_t)kb0 * Mb + min(mb0 + kTileXPW * wave + i, Mb - 1)) * 64 + lane;
+    const size_t xstride = (size_t)Mb * 64;
+    bf16x8_t wr[3][kTileNB], xg[2][kTileXPW];
+    auto load_w = [&](int slot, int st) {
+      const size_t kk = (size_t)min(st, nk - 1);
+#pragma unroll
+      for (int j = 0; j < kTileNB; ++j) wr[slot][j] = wp[j][kk * 64];
     };
+    auto load_x = [&](int slot, int st) {
+      const size_t kk = (size_t)min(st, nk - 1);
 #pragma unroll
-    for (int s0 = 0; s0 < NS - 1; ++s0) issue(s0);
-    for (int st = 0; st < nst; ++st) {
-      __builtin_amdgcn_s_waitcnt(vm_wait((NS - 2) * FPW));  // this wave's loads of stage st have landed
-      __syncthreads();                                      // ... and every wave's; stage st - 1 is free
-      issue(st + NS - 1);
-      const int slot = st % NS;
+      for (int i = 0; i < kTileXPW; ++i) xg[slot][i] = xp[i][kk * xstride];
+    };
+    auto stage_x = [&](int buf, int slot) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        if (st * KS + ks < nk) {
-          bf16x8_t wf[4], xf[4];
+      for (int i = 0; i < kTileXPW; ++i) xs[buf][kTileXPW * wave + i][lane] = xg[slot][i];
+    };
+    // k-step st computes from LDS buffer st % 2 and weight slot st % 3.  Before it, the step loads
+    // W(st + 2), writes X(st + 1) (loaded two steps earlier) into the other LDS buffer and loads X(st + 3);
+    // every wait the compiler inserts is then on loads issued at least one step earlier.
+    load_w(0, 0);
+    load_x(0, 0);
+    load_w(1, 1);
+    load_x(1, 1);
+    stage_x(0, 0);
+    load_x(0, 2);
+    lds_barrier();
+    for (int s0 = 0; s0 < nk; s0 += 6) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) wf[i] = lds[slot][0][4 * wn + i][ks][lane];
+      for (int u = 0; u < 6; ++u) {
+        const int st = s0 + u;
+        load_w((u + 2) % 3, st + 2);
+        stage_x((u + 1) & 1, (u + 1) & 1);
+        load_x((u + 1) & 1, st + 3);
+        if (st < nk) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) xf[j] = lds[slot][1][4 * wm + j][ks][lane];
+          for (int i = 0; i < kTileMB; ++i) {
+            const bf16x8_t xf = xs[u & 1][i][lane];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+            for (int j = 0; j < kTileNB; ++j)
+              acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wr[u % 3][j], xf, acc[j][i], 0, 0, 0);
+          }
+          // two LDS fragment reads ahead of the MFMAs, then one more per group of four
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], xf[j], acc[i][j], 0, 0, 0);
+          for (int i = 0; i < kTileMB - 2; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
         }
+        lds_barrier();
       }
     }
-    __builtin_amdgcn_s_waitcnt(vm_wait(0));  // no load may still be writing LDS when the workgroup ends
   }
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
   float* o = out + (size_t)blockIdx.y * M * N;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int nb = nb0 + 4 * wn + i;
+  for (int j = 0; j < kTileNB; ++j) {
+    const int nb = nb0 + j;
     if (nb >= nbt) continue;
     const int n = nb * 16 + 4 * (lane >> 4);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = (mb0 + 4 * wm + j) * 16 + (lane & 15);
+    for (int i = 0; i < kTileMB; ++i) {
+      const int m = (mb0 + i) * 16 + (lane & 15);
       if (m < M)
-        *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
     }
   }
 }
@@ -434,15 +444,14 @@ int kslice_for(int K, int splits) {
 }
 
 // Tile kernel grid: (padded N tiles) x (M tiles) workgroups in XCD-aware order, K splits in y.
-int tile_groups(int M, int N) {
-  const int Mt = ((M + 15) / 16 + 7) / 8, Nt = (N / 16 + 7) / 8;
-  return (Nt + 7) / 8 * 8 * Mt;
-}
+int tile_m_tiles(int M) { return ((M + 15) / 16 + kTileMB - 1) / kTileMB; }
+int tile_n_tiles(int N) { return (N / 16 + kTileNB * kTileWaves - 1) / (kTileNB * kTileWaves); }
+int tile_groups(int M, int N) { return (tile_n_tiles(N) + 7) / 8 * 8 * tile_m_tiles(M); }
 
 hipError_t launch_tile(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
                        int splits) {
   const dim3 grid(tile_groups(M, N), splits);
-  hipLaunchKernelGGL((k_gemm_tile<2, 2>), grid, dim3(256), 0, s, x, w, out, M, N, K, kslice_for(K, splits));
+  hipLaunchKernelGGL(k_gemm_tile, grid, dim3(64 * kTileWaves), 0, s, x, w, out, M, N, K, kslice_for(K, splits));
   return hipGetLastError();
 }
 
@@ -535,9 +544,9 @@ hipError_t launch_gemm_swiglu_q4(hipStream_t s, const void* X, const void* W, in
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;
   if (M <= kRingMaxRows) return ring_splits(N, K, max_splits);
-  // tile kernel: enough K splits for ~2 workgroups per CU, K slices of at least 512
-  const int nwg = (((M + 15) / 16 + 7) / 8) * ((N / 16 + 7) / 8);
-  int s = (512 + nwg - 1) / nwg;
+  // tile kernel: enough K splits for ~1.5 workgroups per CU, K slices of at least 512
+  const int nwg = tile_m_tiles(M) * tile_n_tiles(N);
+  int s = (384 + nwg - 1) / nwg;
   s = std::min(s, std::max(1, K / 512));
   s = std::max(1, std::min(s, max_splits));
   const int ks = kslice_for(K, s);
