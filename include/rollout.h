@@ -177,6 +177,51 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
                                 int32_t max_new_tokens, float temperature, float top_p,
                                 const float* d_uniforms, int32_t* d_tokens_out);
 
+/*
+ * Completions that end at a stop token, served by continuous batching of
+ * whole groups.  The paper's controller counts T_k, the non-padding tokens a
+ * batch produced (section 4.5, eq. 4), and its runs reward closeness to a
+ * length target (section 5): both presuppose completions that end when the
+ * model draws a stop token.
+ *
+ * Draws are those of rollout_generate (token t of completion s = p * G + g
+ * with d_uniforms[s * max_new_tokens + t]); completion s ends after drawing a
+ * token of the stop set (d_stop_ids, n_stop device int32 ids in [0, vocab);
+ * n_stop = 0: no stop set) or after max_new_tokens tokens.  Outputs (device,
+ * caller-owned): d_tokens_out int32 [n_prompts * G, max_new_tokens], -1 after
+ * the end; d_lengths_out int32 [n_prompts * G], tokens including the stop
+ * token; d_group_step_out int32 [n_prompts] or NULL, the decode step at which
+ * each prompt's group was admitted; *h_decode_steps_out (host, or NULL) the
+ * decode steps run.
+ *
+ * Scheduling: min(seqs_in_flight snapped to whole groups, n_prompts * G)
+ * slots hold groups in prompt order.  Every refill_interval decode steps the
+ * host reads the slots' ended flags; a range whose G completions have all
+ * ended is given the next prompt's group, which is prefilled and draws its
+ * token 0 there.  The call returns when every group has been admitted and has
+ * ended.  Ended completions keep their slot until their whole group ends
+ * (their rows are the padding that T_k excludes).  Errors: EINVAL (bad
+ * argument, or a stop id outside [0, vocab), reported by rollout_sync),
+ * ENOMEM, EDEVICE.
+ */
+rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts,
+                                    int32_t prompt_len, int32_t group_size, int32_t seqs_in_flight,
+                                    int32_t max_new_tokens, float temperature, float top_p,
+                                    const float* d_uniforms, const int32_t* d_stop_ids, int32_t n_stop,
+                                    int32_t refill_interval, int32_t* d_tokens_out, int32_t* d_lengths_out,
+                                    int32_t* d_group_step_out, int32_t* h_decode_steps_out);
+
+/*
+ * Length-target reward of section 5 (its formula is not given; reading:
+ * r = 1 - min(1, |L - target| / target), 1 at the target, 0 at distance
+ * >= target) for n completion lengths d_lengths (device int32), into
+ * d_rewards (device fp32 [n]); *d_total_tokens (device int64, or NULL)
+ * receives the sum of the lengths, the batch's non-padding token count T_k
+ * (section 4.5).  Enqueued on hip_stream.  Errors: EINVAL, EDEVICE.
+ */
+rollout_status rollout_length_rewards(const int32_t* d_lengths, int32_t n, int32_t target, float* d_rewards,
+                                      int64_t* d_total_tokens, void* hip_stream);
+
 /* Wait for the context's stream and report the device error flag (EINVAL if a
  * token id outside [0, vocab) was seen since the last call; the flag is then
  * cleared).  Errors: EINVAL, EDEVICE. */

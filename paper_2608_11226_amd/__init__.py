@@ -24,7 +24,7 @@ _NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", EDEVICE: "EDEVICE", ESTATE: "ESTAT
 EXPORTED = (
     "rollout_plan", "rollout_init", "rollout_prefill", "rollout_decode_step", "rollout_sample",
     "grpo_advantages", "rollout_generate", "rollout_sync", "rollout_destroy", "rollout_last_error",
-    "rollout_export_weight", "rollout_profile_decode_step",
+    "rollout_export_weight", "rollout_profile_decode_step", "rollout_generate_eos", "rollout_length_rewards",
 )
 # include/occupancy.h: power metrics and threshold policy of the occupancy controller (host code)
 EXPORTED_OCC = (
@@ -97,6 +97,9 @@ def _load():
         "rollout_last_error": ([vp], ctypes.c_char_p),
         "rollout_export_weight": ([vp, i32, vp], i32),
         "rollout_profile_decode_step": ([vp, vp, vp, ctypes.POINTER(StepProfile)], i32),
+        "rollout_generate_eos": ([vp, vp, i32, i32, i32, i32, i32, f32, f32, vp, vp, i32, i32, vp, vp, vp,
+                                  ctypes.POINTER(i32)], i32),
+        "rollout_length_rewards": ([vp, i32, i32, vp, vp, vp], i32),
         "occ_rolling_mean": ([vp, ctypes.c_int64, f64, f64, vp], i32),
         "occ_violation": ([vp, ctypes.c_int64, f64, f64, ctypes.POINTER(f64), ctypes.POINTER(f64)], i32),
         "occ_normalize_budget": ([f64, f64, f64], f64),
@@ -168,6 +171,22 @@ def rollout_generate(ctx, prompts, n_prompts: int, prompt_len: int, group_size: 
                      max_new_tokens: int, temperature: float, top_p: float, uniforms, tokens_out):
     _check(lib.rollout_generate(ctx, _ptr(prompts), n_prompts, prompt_len, group_size, seqs_in_flight,
                                 max_new_tokens, temperature, top_p, _ptr(uniforms), _ptr(tokens_out)), ctx)
+
+
+def rollout_generate_eos(ctx, prompts, n_prompts: int, prompt_len: int, group_size: int, seqs_in_flight: int,
+                         max_new_tokens: int, temperature: float, top_p: float, uniforms, stop_ids, n_stop: int,
+                         refill_interval: int, tokens_out, lengths_out, group_step_out=None) -> int:
+    """Returns the number of decode steps run."""
+    steps = ctypes.c_int32(0)
+    _check(lib.rollout_generate_eos(ctx, _ptr(prompts), n_prompts, prompt_len, group_size, seqs_in_flight,
+                                    max_new_tokens, temperature, top_p, _ptr(uniforms), _ptr(stop_ids), n_stop,
+                                    refill_interval, _ptr(tokens_out), _ptr(lengths_out), _ptr(group_step_out),
+                                    ctypes.byref(steps)), ctx)
+    return steps.value
+
+
+def rollout_length_rewards(lengths, n: int, target: int, rewards, total_tokens=None, stream=None):
+    _check(lib.rollout_length_rewards(_ptr(lengths), n, target, _ptr(rewards), _ptr(total_tokens), _ptr(stream)))
 
 
 def rollout_sync(ctx):

@@ -122,6 +122,23 @@ hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, 
 hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
                               void* dst);
 hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);
+// Continuous batching (batching.hip): per-slot completion index, next token column, ended flag, the
+// slot's last draw and its staged uniform; all [S] in the arena.
+struct CbState {
+  int32_t* seq;
+  int32_t* col;
+  int32_t* done;
+  int32_t* draw;
+  float* u_slot;
+};
+hipError_t launch_stop_bitmap(hipStream_t s, uint32_t* bitmap, int V, const int32_t* ids, int n, int32_t* err);
+hipError_t launch_cb_reset(hipStream_t s, int S, const CbState& cb);
+hipError_t launch_cb_admit(hipStream_t s, const CbState& cb, int r0, int G, int seq0, int P, int N,
+                           int32_t* ctx_len, int32_t* tokens_out);
+hipError_t launch_cb_commit(hipStream_t s, const CbState& cb, int r0, int r1, int N, const uint32_t* stop,
+                            const float* u, int32_t* ctx_len, int32_t* tokens_out, int32_t* lengths, bool advance);
+hipError_t launch_length_rewards(hipStream_t s, const int32_t* lengths, int n, int target, float* rewards,
+                                 long long* total);
 hipError_t launch_set_cols(hipStream_t s, int32_t* cols, int c0, int c1);
 // Sampler scratch: stored e values of S rows plus per-chunk statistics.
 size_t sample_scratch_bytes(int S, int V);

@@ -42,6 +42,7 @@ struct Layout {
   size_t weights_end = 0;  // weights + rope tables
   size_t x = 0, a = 0, q = 0, o = 0, h = 0, a_last = 0, part = 0, opart = 0, ml = 0, logits = 0;
   size_t tables = 0, ctx_len = 0, cols = 0, err = 0, samp = 0, wdq = 0;
+  size_t cb = 0, stopmap = 0;  // continuous batching: 5 x [S] slot state, then the stop-token bitmap
   size_t work_end = 0;     // start of the KV pool
   size_t weight_bytes = 0, work_bytes = 0, kv_block_bytes = 0;
   int S = 0, R = 0, T_chunk = 0, max_blocks = 0, attn_splits_max = 1;
@@ -191,6 +192,8 @@ Layout make_layout(const Dims& D, int S, int max_prompt_len) {
   Lo.ctx_len = Lo.tables + (size_t)S * Lo.max_blocks * 4;
   Lo.cols = take(64);
   Lo.err = take(64);
+  Lo.cb = take((size_t)5 * S * 4);
+  Lo.stopmap = take((size_t)(D.V + 31) / 32 * 4);
   // int4: batches above the ring GEMM's rows multiply bf16 hi and lo copies of one projection at a time
   if (D.wq4)
     Lo.wdq = take(std::max(std::max((size_t)D.nqkv * D.d, (size_t)D.d * D.qd), (size_t)2 * D.ff * D.d) * 4);
@@ -229,6 +232,7 @@ struct rollout_ctx {
 
   // host staging (pinned) for block tables and context lengths
   int32_t* h_tables = nullptr;
+  int32_t* h_done = nullptr;  // ended flags of the slots, read back at refill boundaries
 
   // current wave
   bool wave = false;
@@ -477,11 +481,12 @@ rollout_status upload_wave(rollout_ctx* c, int n_prompts, int P, int G) {
   return ROLLOUT_OK;
 }
 
-rollout_status do_prefill(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G, float* d_logits) {
+// Prefill n_prompts prompts whose groups occupy the slots from row0 on (G rows each, block tables already
+// in place); the last position's logits, replicated per sequence, go to d_logits [n_prompts * G, V].
+rollout_status prefill_rows(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G, int row0,
+                            float* d_logits) {
   const Dims& D = c->D;
   const Layout& Lo = c->Lo;
-  rollout_status r = upload_wave(c, n_prompts, P, G);
-  if (r) return r;
   const int per_chunk = std::max(1, Lo.T_chunk / P);
   for (int p0 = 0; p0 < n_prompts; p0 += per_chunk) {
     const int np = std::min(per_chunk, n_prompts - p0);
@@ -491,8 +496,8 @@ rollout_status do_prefill(rollout_ctx* c, const int32_t* d_prompts, int n_prompt
       HIP_TRY(c, launch_embed(c->stream, D.dtype, c->at(Lo.embed), d_prompts + (size_t)p0 * P, 1, nullptr, M, D.d, D.V,
                               c->at<float>(Lo.x), c->at<int32_t>(Lo.err)), "embed");
     }
-    RowMap rm{nullptr, P, G, p0 * G};
-    r = forward_layers(c, M, rm, P, (double)np * P * (P + 1) / 2.0);
+    RowMap rm{nullptr, P, G, row0 + p0 * G};
+    rollout_status r = forward_layers(c, M, rm, P, (double)np * P * (P + 1) / 2.0);
     if (r) return r;
     HIP_TRY(c, launch_gather_rows(c->stream, D.dtype, c->at(Lo.a), D.d, P, G, np, c->at(Lo.a_last)), "gather");
     int s;
@@ -502,9 +507,15 @@ rollout_status do_prefill(rollout_ctx* c, const int32_t* d_prompts, int n_prompt
   return ROLLOUT_OK;
 }
 
+rollout_status do_prefill(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G, float* d_logits) {
+  rollout_status r = upload_wave(c, n_prompts, P, G);
+  if (r) return r;
+  return prefill_rows(c, d_prompts, n_prompts, P, G, 0, d_logits);
+}
+
 // Enqueue one decode step of the current wave (no host-side state change).
 rollout_status enqueue_decode(rollout_ctx* c, const int32_t* tokens, int tok_stride, const int32_t* col,
-                              float* d_logits, int ctx_max) {
+                              float* d_logits, int ctx_max, bool advance = true) {
   const Dims& D = c->D;
   const Layout& Lo = c->Lo;
   const int S = c->S;
@@ -519,7 +530,7 @@ rollout_status enqueue_decode(rollout_ctx* c, const int32_t* tokens, int tok_str
   int s;
   r = gemm(c, c->at(Lo.a), c->at(Lo.lm_head), d_logits, S, D.V, D.d, 1, &s);
   if (r) return r;
-  HIP_TRY(c, launch_advance(c->stream, c->at<int32_t>(Lo.ctx_len), S, nullptr), "advance");
+  if (advance) HIP_TRY(c, launch_advance(c->stream, c->at<int32_t>(Lo.ctx_len), S, nullptr), "advance");
   return ROLLOUT_OK;
 }
 
@@ -623,6 +634,7 @@ rollout_status rollout_init(const rollout_model_config* cfg, void* d_arena, uint
     c->own_stream = true;
   }
   hipError_t e = hipHostMalloc((void**)&c->h_tables, (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_done, (size_t)Lo.S * 4, hipHostMallocDefault);
   if (e != hipSuccess) {
     rollout_destroy(c);
     return fail(nullptr, ROLLOUT_EDEVICE, std::string("pinned staging: ") + hipGetErrorString(e));
@@ -673,6 +685,7 @@ void rollout_destroy(rollout_ctx* ctx) {
   if (ctx->stream) hipStreamSynchronize(ctx->stream);
   for (hipEvent_t e : ctx->prof.ev) hipEventDestroy(e);
   if (ctx->h_tables) hipHostFree(ctx->h_tables);
+  if (ctx->h_done) hipHostFree(ctx->h_done);
   if (ctx->own_stream) hipStreamDestroy(ctx->stream);
   delete ctx;
 }
@@ -812,6 +825,145 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
     hipGraphExecDestroy(exec);
     if (se != hipSuccess) return hip_fail(ctx, se, "stream sync");
   }
+  return ROLLOUT_OK;
+}
+
+rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts,
+                                    int32_t prompt_len, int32_t group_size, int32_t seqs_in_flight,
+                                    int32_t max_new_tokens, float temperature, float top_p, const float* d_uniforms,
+                                    const int32_t* d_stop_ids, int32_t n_stop, int32_t refill_interval,
+                                    int32_t* d_tokens_out, int32_t* d_lengths_out, int32_t* d_group_step_out,
+                                    int32_t* h_decode_steps_out) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!d_prompts || !d_uniforms || !d_tokens_out || !d_lengths_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
+  if (n_stop < 0 || (n_stop > 0 && !d_stop_ids)) return fail(ctx, ROLLOUT_EINVAL, "n_stop < 0 or stop ids NULL");
+  if (refill_interval < 1) return fail(ctx, ROLLOUT_EINVAL, "refill_interval must be >= 1");
+  if (n_prompts < 1 || group_size < 1 || seqs_in_flight < 1)
+    return fail(ctx, ROLLOUT_EINVAL, "n_prompts, group_size and seqs_in_flight must be >= 1");
+  if (prompt_len < 1 || prompt_len > ctx->cfg.max_prompt_len)
+    return fail(ctx, ROLLOUT_EINVAL, "prompt_len must be in [1, max_prompt_len]");
+  if (max_new_tokens < 1 || max_new_tokens > ctx->cfg.max_new_tokens)
+    return fail(ctx, ROLLOUT_EINVAL, "max_new_tokens must be in [1, config max_new_tokens]");
+  if (!(temperature >= 0.f) || !std::isfinite(temperature)) return fail(ctx, ROLLOUT_EINVAL, "temperature must be >= 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(ctx, ROLLOUT_EINVAL, "top_p must be in (0, 1]");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  const int G = group_size, P = prompt_len, N = max_new_tokens;
+  // slots: whole groups, within the context's rows and the KV pool, no more ranges than prompts
+  int S = std::min<int64_t>(seqs_in_flight, Lo.S) / G * G;
+  const int ctxlen = P + ctx->cfg.max_new_tokens;
+  while (S >= G && blocks_needed(S / G, G, P, ctxlen, D.blk) > ctx->n_blocks) S -= G;
+  if (S < G) return fail(ctx, ROLLOUT_ENOMEM, "one group does not fit in the context");
+  const int ranges = std::min(S / G, (int)n_prompts);
+  S = ranges * G;
+  // every range keeps its block-table rows for the whole call; a refilled range reuses them
+  ctx->wave = false;
+  rollout_status r = upload_wave(ctx, ranges, P, G);
+  if (r) return r;
+  int32_t* base = ctx->at<int32_t>(Lo.cb);
+  const CbState cb{base, base + S, base + 2 * S, base + 3 * S, reinterpret_cast<float*>(base + 4 * S)};
+  uint32_t* stop = n_stop > 0 ? ctx->at<uint32_t>(Lo.stopmap) : nullptr;
+  if (stop) HIP_TRY(ctx, launch_stop_bitmap(ctx->stream, stop, D.V, d_stop_ids, n_stop, ctx->at<int32_t>(Lo.err)), "stop set");
+  HIP_TRY(ctx, launch_cb_reset(ctx->stream, S, cb), "slot reset");
+  float* logits = ctx->at<float>(Lo.logits);
+  int32_t* ctx_len = ctx->at<int32_t>(Lo.ctx_len);
+  void* samp = ctx->at(Lo.samp);
+  std::vector<int> range_group(ranges, -1);
+  std::vector<int32_t> admit_step(n_prompts, -1);
+  int next = 0;
+  // a range takes the next prompt's group: reset its slots, prefill, draw token 0 from the prefill logits
+  auto admit = [&](int k, int boundary) -> rollout_status {
+    const int p = next++;
+    const int r0 = k * G, seq0 = p * G;
+    admit_step[p] = boundary;
+    range_group[k] = p;
+    HIP_TRY(ctx, launch_cb_admit(ctx->stream, cb, r0, G, seq0, P, N, ctx_len, d_tokens_out), "admit");
+    rollout_status rr = prefill_rows(ctx, d_prompts + (size_t)p * P, 1, P, G, r0, logits);
+    if (rr) return rr;
+    HIP_TRY(ctx, launch_sample(ctx->stream, logits, G, D.V, temperature, top_p, d_uniforms + (size_t)seq0 * N, N,
+                               nullptr, cb.draw + r0, 1, samp), "sample");
+    HIP_TRY(ctx, launch_cb_commit(ctx->stream, cb, r0, r0 + G, N, stop, d_uniforms, ctx_len, d_tokens_out,
+                                  d_lengths_out, false), "commit");
+    return ROLLOUT_OK;
+  };
+  // one decode step over all slots: feed each slot's last draw, draw with its staged uniform, file the draws
+  auto step = [&]() -> rollout_status {
+    rollout_status rr = enqueue_decode(ctx, cb.draw, 1, nullptr, logits, P + N, false);
+    if (rr) return rr;
+    HIP_TRY(ctx, launch_sample(ctx->stream, logits, S, D.V, temperature, top_p, cb.u_slot, 1, nullptr, cb.draw, 1,
+                               samp), "sample");
+    HIP_TRY(ctx, launch_cb_commit(ctx->stream, cb, 0, S, N, stop, d_uniforms, ctx_len, d_tokens_out, d_lengths_out,
+                                  true), "commit");
+    return ROLLOUT_OK;
+  };
+  for (int k = 0; k < ranges; ++k)
+    if ((r = admit(k, 0))) return r;
+  hipGraphExec_t exec = nullptr;
+  auto finish = [&](rollout_status st) {
+    if (exec) {
+      hipStreamSynchronize(ctx->stream);
+      hipGraphExecDestroy(exec);
+    }
+    return st;
+  };
+  if (!ctx->prof.on) {
+    hipGraph_t graph = nullptr;
+    HIP_TRY(ctx, hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal), "begin capture");
+    r = step();
+    hipError_t ce = hipStreamEndCapture(ctx->stream, &graph);
+    if (r) {
+      if (graph) hipGraphDestroy(graph);
+      return r;
+    }
+    if (ce != hipSuccess) return hip_fail(ctx, ce, "end capture");
+    hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    hipGraphDestroy(graph);
+    if (ie != hipSuccess) return hip_fail(ctx, ie, "graph instantiate");
+  }
+  int steps = 0;
+  auto live = [&]() {
+    for (int k = 0; k < ranges; ++k)
+      if (range_group[k] >= 0) return true;
+    return false;
+  };
+  while (live()) {
+    for (int i = 0; i < refill_interval; ++i) {
+      if (exec) {
+        hipError_t le = hipGraphLaunch(exec, ctx->stream);
+        if (le != hipSuccess) return finish(hip_fail(ctx, le, "graph launch"));
+      } else if ((r = step())) {
+        return finish(r);
+      }
+    }
+    steps += refill_interval;
+    hipError_t ce = hipMemcpyAsync(ctx->h_done, cb.done, (size_t)S * 4, hipMemcpyDeviceToHost, ctx->stream);
+    if (ce == hipSuccess) ce = hipStreamSynchronize(ctx->stream);
+    if (ce != hipSuccess) return finish(hip_fail(ctx, ce, "ended flags read"));
+    for (int k = 0; k < ranges; ++k) {
+      if (range_group[k] < 0) continue;
+      bool ended = true;
+      for (int g = 0; g < G; ++g) ended = ended && ctx->h_done[k * G + g] != 0;
+      if (!ended) continue;
+      range_group[k] = -1;
+      if (next < n_prompts && (r = admit(k, steps))) return finish(r);
+    }
+  }
+  r = finish(ROLLOUT_OK);
+  exec = nullptr;
+  if (d_group_step_out)
+    HIP_TRY(ctx, hipMemcpy(d_group_step_out, admit_step.data(), (size_t)n_prompts * 4, hipMemcpyHostToDevice),
+            "group steps");
+  if (h_decode_steps_out) *h_decode_steps_out = steps;
+  return r;
+}
+
+rollout_status rollout_length_rewards(const int32_t* d_lengths, int32_t n, int32_t target, float* d_rewards,
+                                      int64_t* d_total_tokens, void* hip_stream) {
+  if (!d_lengths || !d_rewards) return fail(nullptr, ROLLOUT_EINVAL, "lengths and rewards must be non-NULL");
+  if (n < 1 || target < 1) return fail(nullptr, ROLLOUT_EINVAL, "n and target must be >= 1");
+  hipError_t e = launch_length_rewards((hipStream_t)hip_stream, d_lengths, n, target, d_rewards,
+                                       reinterpret_cast<long long*>(d_total_tokens));
+  if (e != hipSuccess) return fail(nullptr, ROLLOUT_EDEVICE, std::string("length rewards: ") + hipGetErrorString(e));
   return ROLLOUT_OK;
 }
 

@@ -1,0 +1,141 @@
+"""GPU parity of stop-token completions under continuous batching (rollout_generate_eos) and of the
+length-target reward, through the C ABI, against oracle/batching.py."""
+import numpy as np
+import pytest
+
+import paper_2608_11226_amd as R
+import workload as W
+from gpu_helpers import guarded_token_compare, log, shape_of, to_dev
+from oracle import OracleModel, rollout
+from oracle.batching import continuous_schedule, length_target_reward, rollout_eos
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+SMALL_BF16 = (2, 256, 8, 2, 64, 512, 2048, 1e6)
+
+
+def _run_eos(eng, prompts, G, slots, N, T, top_p, u, stop, refill):
+    n_prompts, P = prompts.shape
+    S = n_prompts * G
+    dev = "cuda:0"
+    tokens = torch.full((S, N), -7, dtype=torch.int32, device=dev)
+    lengths = torch.full((S,), -7, dtype=torch.int32, device=dev)
+    gstep = torch.full((n_prompts,), -7, dtype=torch.int32, device=dev)
+    stop_t = to_dev(np.asarray(stop, dtype=np.int32), torch) if len(stop) else torch.zeros(1, dtype=torch.int32,
+                                                                                            device=dev)
+    steps = R.rollout_generate_eos(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, slots, N, T, top_p,
+                                   to_dev(u, torch), stop_t, len(stop), refill, tokens, lengths, gstep)
+    eng.synchronize()
+    return tokens.cpu().numpy(), lengths.cpu().numpy(), gstep.cpu().numpy(), steps
+
+
+def _check_structure(tokens, lengths, stop, N, V):
+    stop = set(int(s) for s in stop)
+    for s in range(tokens.shape[0]):
+        L = int(lengths[s])
+        assert 1 <= L <= N
+        assert np.all(tokens[s, L:] == -1), f"completion {s} not padded after its end"
+        body = tokens[s, :L]
+        assert np.all((body >= 0) & (body < V))
+        hits = [t for t in range(L) if int(body[t]) in stop]
+        # ends at its first stop token, or runs to max_new_tokens without one
+        assert (hits and hits[0] == L - 1) or (not hits and L == N), f"completion {s}: stop rule"
+
+
+@pytest.mark.parametrize("T,top_p,refill", [(1.0, 1.0, 1), (0.8, 0.9, 3), (0.0, 1.0, 2)])
+def test_tiny_fp32_eos_matches_oracle(T, top_p, refill):
+    G, n_prompts, P, N, slots = 4, 5, 12, 16, 8
+    log(f"tiny fp32 eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill}, T={T} top_p={top_p}")
+    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, slots)
+    eng = R.Engine(cfg, group_size=G)
+    model = OracleModel(shape_of(cfg), mode="fp32")
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=51)
+    u = W.uniforms(n_prompts * G, N, seed=52)
+    plain = rollout(model, prompts, G, N, T, top_p, u, keep_logits=False)["tokens"]
+    # stop tokens taken from the draws themselves so that the completions end at different lengths
+    stop = sorted({int(plain[0, 2]), int(plain[5, 6]), int(plain[9, 0]), int(plain[14, 11])})
+    ref = rollout_eos(model, prompts, G, N, T, top_p, u, stop)
+    tok, L, gstep, steps = _run_eos(eng, prompts, G, slots, N, T, top_p, u, stop, refill)
+    _check_structure(tok, L, stop, N, cfg.vocab)
+    compared, skipped = guarded_token_compare(tok, np.where(ref["tokens"] < 0, -1, ref["tokens"]), ref["margins"])
+    log(f"  lengths {L.tolist()}; compared {compared} tokens, skipped {skipped} after near-ties")
+    exact = [s for s in range(n_prompts * G) if np.all(ref["margins"][s, :ref["lengths"][s]] >= 1e-5)]
+    for s in exact:
+        assert L[s] == ref["lengths"][s], f"completion {s}: length {L[s]} oracle {ref['lengths'][s]}"
+    assert compared >= 60 and len(exact) >= n_prompts * G // 2
+    # the schedule follows the refill rule for the lengths the device produced
+    sch = continuous_schedule(L, G, slots // G, refill)
+    assert list(gstep) == list(sch["admit"]) and steps == sch["steps"], (gstep, sch)
+    assert len(set(gstep.tolist())) > 1, "no refill happened"
+    eng.close()
+
+
+def test_tiny_fp32_eos_without_stop_set_equals_generate():
+    G, n_prompts, P, N = 2, 4, 16, 12
+    log("tiny fp32 eos with an empty stop set against rollout_generate")
+    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, 8)
+    eng = R.Engine(cfg, group_size=G)
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=21)
+    u = W.uniforms(n_prompts * G, N, seed=22)
+    tok, L, gstep, steps = _run_eos(eng, prompts, G, 8, N, 0.8, 0.9, u, [], 4)
+    assert np.all(L == N) and list(gstep) == [0] * n_prompts and steps == 12
+    out = torch.full((n_prompts * G, N), -1, dtype=torch.int32, device="cuda:0")
+    R.rollout_generate(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, 8, N, 0.8, 0.9, to_dev(u, torch), out)
+    eng.synchronize()
+    assert np.array_equal(out.cpu().numpy(), tok)
+    eng.close()
+
+
+@pytest.mark.parametrize("refill,slots", [(1, 8), (4, 16), (2, 4)])
+def test_bf16_eos_schedule_and_stop_rule(refill, slots):
+    G, n_prompts, P, N = 4, 7, 40, 24
+    log(f"bf16 small GQA eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill}")
+    cfg = R.model_config(SMALL_BF16, R.DTYPE_BF16, P, N, slots)
+    eng = R.Engine(cfg, group_size=G)
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=61)
+    u = W.uniforms(n_prompts * G, N, seed=62)
+    stop = list(range(0, cfg.vocab, 16))  # 1 in 16 ids: random-init completions end after ~16 tokens
+    tok, L, gstep, steps = _run_eos(eng, prompts, G, slots, N, 1.0, 1.0, u, stop, refill)
+    _check_structure(tok, L, stop, N, cfg.vocab)
+    log(f"  lengths mean {L.mean():.1f} min {L.min()} max {L.max()}; {steps} decode steps")
+    sch = continuous_schedule(L, G, min(slots // G, n_prompts), refill)
+    assert list(gstep) == list(sch["admit"]) and steps == sch["steps"]
+    assert L.min() < N and len(set(L.tolist())) > 3
+    # token 0 of every completion is drawn from its prompt's prefill logits: the same as rollout_generate's
+    out = torch.full((n_prompts * G, N), -1, dtype=torch.int32, device="cuda:0")
+    R.rollout_generate(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, slots, N, 1.0, 1.0, to_dev(u, torch), out)
+    eng.synchronize()
+    same0 = float(np.mean(out.cpu().numpy()[:, 0] == tok[:, 0]))
+    log(f"  token 0 agreement with rollout_generate: {same0:.2f}")
+    assert same0 >= 0.9
+    eng.close()
+
+
+def test_length_rewards_and_token_total():
+    rng = np.random.default_rng(3)
+    L = rng.integers(1, 400, size=300).astype(np.int32)
+    rew = torch.empty(300, dtype=torch.float32, device="cuda:0")
+    tot = torch.zeros(1, dtype=torch.int64, device="cuda:0")
+    R.rollout_length_rewards(to_dev(L, torch), 300, 128, rew, tot)
+    torch.cuda.synchronize()
+    want = length_target_reward(L, 128).astype(np.float32)
+    assert np.array_equal(rew.cpu().numpy(), want)
+    assert int(tot.item()) == int(L.sum())
+
+
+def test_bad_stop_id_is_reported():
+    cfg = R.model_config("tiny", R.DTYPE_FP32, 8, 4, 4)
+    eng = R.Engine(cfg, group_size=2)
+    prompts = W.prompts(2, 8, cfg.vocab)
+    u = W.uniforms(4, 4)
+    dev = "cuda:0"
+    tokens = torch.empty((4, 4), dtype=torch.int32, device=dev)
+    lengths = torch.empty(4, dtype=torch.int32, device=dev)
+    stop = torch.tensor([3, cfg.vocab + 9], dtype=torch.int32, device=dev)
+    R.rollout_generate_eos(eng.ctx, to_dev(prompts, torch), 2, 8, 2, 4, 4, 1.0, 1.0, to_dev(u, torch), stop, 2, 1,
+                           tokens, lengths)
+    with pytest.raises(R.RolloutError, match="outside"):
+        eng.synchronize()
+    eng.close()
