@@ -17,8 +17,8 @@
 // computes the current one; at the end the waves merge their (max, sum,
 // output) states through LDS and write the normalised output directly in the
 // O-projection's operand layout, so no partial results leave the workgroup.
-// K and V are read once per row and KV head.  P is rounded to bf16 for the
-// MFMA (scores, softmax and accumulation are fp32).
+// K and V are read once per row and KV head.  P enters the MFMA as the sum of
+// two bf16 terms (scores, softmax and accumulation are fp32).
 //
 // fp32 path (and head_dim 32): a VALU kernel split over the context that
 // stages K/V tiles in LDS; a combine kernel merges its splits with
@@ -113,11 +113,19 @@ __device__ __forceinline__ void attend_tile(KVTile<HD>& t, const bf16x8_t* qf, i
       for (int e = 0; e < 4; ++e)
         if (e >= vm) t.v[j][e] = 0;
   }
-  const short4_t pf = {f2bs(p[0]), f2bs(p[1]), f2bs(p[2]), f2bs(p[3])};
+  // p enters the MFMA as hi + lo, two bf16 terms whose sum is p to about 2^-17 relative: a single bf16
+  // rounding of p would be an extra rounding point, worth up to ~2.5e-2 in the logits at 7B width
+  short4_t ph, pl;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ph[i] = f2bs(p[i]);
+    pl[i] = f2bs(p[i] - __uint_as_float((uint32_t)(uint16_t)ph[i] << 16));
+  }
 #pragma unroll
   for (int j = 0; j < HD / 16; ++j) {
     o[j] *= alpha;
-    o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(t.v[j], pf, o[j], 0, 0, 0);
+    o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(t.v[j], ph, o[j], 0, 0, 0);
+    o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(t.v[j], pl, o[j], 0, 0, 0);
   }
 }
 
