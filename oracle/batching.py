@@ -14,14 +14,19 @@ taken here (listed in the design notes as well):
   uniform u[s, t]) and ends after drawing a token of the stop set, which is
   kept as its last token, or after ``max_new_tokens`` tokens.  Its length L
   counts the stop token; positions t >= L hold the pad value -1.
-* Continuous batching.  ``seqs_in_flight`` slots hold whole groups (section
-  4.3 keeps the batch a multiple of G).  Groups are admitted in prompt order.
-  The host inspects the slots every ``refill_interval`` decode steps; a slot
-  range whose G completions have all ended is given the next prompt's group,
-  which is prefilled and draws its token 0 at that boundary.  The rollout ends
-  at the first boundary where every group has been admitted and has ended.
-  Per completion the tokens do not depend on the schedule: only its prompt,
-  its own uniforms and the model enter them.
+* Continuous batching.  ``seqs_in_flight`` slots are refilled as completions
+  end; the host inspects them every ``refill_interval`` decode steps (the
+  boundaries are the multiples of R).  Two granularities:
+  - whole groups: slot ranges of G hold one group each (section 4.3 keeps the
+    batch a multiple of G); a range whose G completions have all ended takes
+    the next prompt's group, which is prefilled and draws its token 0 there;
+  - single completions: a slot whose completion has ended takes the next
+    completion in order s = p * G + g (a group's prompt is prefilled when its
+    first completion is admitted, and every member draws token 0 from those
+    logits); freed slots are filled in slot order.
+  The rollout ends at the first boundary where everything has been admitted
+  and has ended.  Per completion the tokens do not depend on the schedule:
+  only its prompt, its own uniforms and the model enter them.
 * Length-target reward.  r = 1 - min(1, |L - L*| / L*) for target L*: 1 at
   the target, falling linearly to 0 at distance L*.
 
@@ -29,6 +34,8 @@ Parity: ``rollout_eos`` is pinned against the plain rollout truncated at the
 first stop token (an independent code path) and against the empty and full
 stop sets; ``continuous_schedule`` against a step-by-step simulation of the
 slots and hand-worked schedules (``tests/golden/batching_schedule.txt``);
+``sequence_schedule`` against ``simulate_sequence_slots`` (a step simulation that
+also tracks each group's prompt record) and a hand-worked case;
 ``length_target_reward`` against its closed-form points.  All in
 ``tests/test_oracle_batching.py``.
 """
@@ -76,6 +83,16 @@ def rollout_eos(model, prompts: np.ndarray, group_size: int, max_new_tokens: int
                 logits = model.decode(cache, tok)
             lengths[s] = t
     return {"tokens": tokens, "lengths": lengths, "margins": margins}
+
+
+def sequence_schedule(lengths, slots: int, refill_interval: int) -> dict:
+    """Single-completion refill: admission and release boundary of every completion, and the steps in all.
+
+    Same rule as ``continuous_schedule`` with ranges of one completion: a completion admitted at b ends
+    at step b + L - 1 and its slot is seen free at b + R * max(1, ceil((L - 1) / R)).
+    """
+    lengths = np.asarray(lengths).reshape(-1)
+    return continuous_schedule(lengths, 1, slots, refill_interval)
 
 
 def continuous_schedule(lengths, group_size: int, slot_groups: int, refill_interval: int) -> dict:
@@ -161,6 +178,59 @@ def simulate_slots(lengths, group_size: int, slot_groups: int, refill_interval: 
                 if nxt < n_groups:
                     admit_into(k, step)
     return {"admit": admit, "free": free, "steps": step}
+
+
+def simulate_sequence_slots(lengths, group_size: int, slots: int, refill_interval: int) -> dict:
+    """Step-by-step simulation of single-completion refill, tracking groups and their prompt records.
+
+    Besides the schedule it reports the most prompt records (a group's shared prompt cache, alive from
+    its first admission until its last completion ends) held at once, which sizes the KV pool.
+    """
+    lengths = np.asarray(lengths).reshape(-1)
+    n = lengths.size
+    R = int(refill_interval)
+    slot = [-1] * slots
+    drawn = [0] * slots
+    admit = np.full(n, -1, dtype=np.int64)
+    free = np.full(n, -1, dtype=np.int64)
+    ended = {}
+    live_groups = set()
+    most = 0
+    nxt = 0
+
+    def admit_into(r, step):
+        nonlocal nxt, most
+        s = nxt
+        nxt += 1
+        admit[s] = step
+        slot[r] = s
+        drawn[r] = 1
+        live_groups.add(s // group_size)
+        most = max(most, len(live_groups))
+
+    for r in range(slots):
+        if nxt < n:
+            admit_into(r, 0)
+    step = 0
+    while any(x >= 0 for x in slot):
+        for _ in range(R):
+            step += 1
+            for r in range(slots):
+                if slot[r] >= 0 and drawn[r] < lengths[slot[r]]:
+                    drawn[r] += 1
+        for r in range(slots):
+            s = slot[r]
+            if s < 0 or drawn[r] < lengths[s]:
+                continue
+            free[s] = step
+            slot[r] = -1
+            p = s // group_size
+            ended[p] = ended.get(p, 0) + 1
+            if ended[p] == group_size:
+                live_groups.discard(p)
+            if nxt < n:
+                admit_into(r, step)
+    return {"admit": admit, "free": free, "steps": step, "most_records": most}
 
 
 def length_target_reward(lengths, target: int = 128) -> np.ndarray:

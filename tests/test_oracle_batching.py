@@ -5,7 +5,8 @@ import pytest
 import workload as W
 from conftest import read_golden
 from oracle import OracleModel, rollout
-from oracle.batching import PAD, continuous_schedule, length_target_reward, rollout_eos, simulate_slots
+from oracle.batching import (PAD, continuous_schedule, length_target_reward, rollout_eos, sequence_schedule,
+                             simulate_sequence_slots, simulate_slots)
 
 
 def _ints(s):
@@ -93,3 +94,29 @@ def test_length_target_reward_closed_form():
     want = np.array([1.0, 0.5, 0.5, 0.0, 1.0 / 128.0, 0.0, 0.0])
     assert np.allclose(length_target_reward(L, 128), want, rtol=0, atol=1e-15)
     assert length_target_reward([10], 10)[0] == 1.0 and length_target_reward([15], 10)[0] == 0.5
+
+
+def test_single_completion_schedule_equals_simulation():
+    rng = np.random.default_rng(9)
+    for _ in range(200):
+        G = int(rng.choice([1, 2, 4, 8]))
+        n = G * int(rng.integers(1, 7))
+        slots = int(rng.integers(1, 12))
+        R = int(rng.choice([1, 2, 5]))
+        lengths = rng.integers(1, 30, size=n)
+        a = sequence_schedule(lengths, slots, R)
+        b = simulate_sequence_slots(lengths, G, slots, R)
+        assert np.array_equal(a["admit"], b["admit"]) and np.array_equal(a["free"], b["free"])
+        assert a["steps"] == b["steps"]
+        # a live prompt record per group with a completion in a slot, plus one being admitted
+        assert b["most_records"] <= min(slots, n) + 1
+
+
+def test_single_completion_schedule_hand_worked():
+    # slots 2, R 1, lengths 3,1,2,2: s0 -> slot 0 (ends step 2), s1 -> slot 1 (ends at 0, seen at 1)
+    # step 1: slot 1 -> s2 (ends 1 + 1 = 2); step 2: slot 0 -> s3 (ends 3), slot 1 seen free (s2); step 3: s3 seen
+    got = sequence_schedule([3, 1, 2, 2], 2, 1)
+    assert list(got["admit"]) == [0, 0, 1, 2] and list(got["free"]) == [2, 1, 2, 3] and got["steps"] == 3
+    # fewer decode steps than refilling whole groups of 2 over the same slots
+    assert continuous_schedule([3, 1, 2, 2], 2, 1, 1)["steps"] == 3
+    assert sequence_schedule([5, 1, 1, 5, 1, 1], 2, 1)["steps"] < continuous_schedule([5, 1, 1, 5, 1, 1], 2, 1, 1)["steps"]
