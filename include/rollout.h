@@ -178,11 +178,11 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
                                 const float* d_uniforms, int32_t* d_tokens_out);
 
 /*
- * Completions that end at a stop token, served by continuous batching of
- * whole groups.  The paper's controller counts T_k, the non-padding tokens a
- * batch produced (section 4.5, eq. 4), and its runs reward closeness to a
- * length target (section 5): both presuppose completions that end when the
- * model draws a stop token.
+ * Completions that end at a stop token, served by continuous batching.  The
+ * paper's controller counts T_k, the non-padding tokens a batch produced
+ * (section 4.5, eq. 4), and its runs reward closeness to a length target
+ * (section 5): both presuppose completions that end when the model draws a
+ * stop token.
  *
  * Draws are those of rollout_generate (token t of completion s = p * G + g
  * with d_uniforms[s * max_new_tokens + t]); completion s ends after drawing a
@@ -190,26 +190,36 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
  * n_stop = 0: no stop set) or after max_new_tokens tokens.  Outputs (device,
  * caller-owned): d_tokens_out int32 [n_prompts * G, max_new_tokens], -1 after
  * the end; d_lengths_out int32 [n_prompts * G], tokens including the stop
- * token; d_group_step_out int32 [n_prompts] or NULL, the decode step at which
- * each prompt's group was admitted; *h_decode_steps_out (host, or NULL) the
+ * token; d_admit_step_out int32 [n_prompts * G] or NULL, the decode step at
+ * which each completion was admitted; *h_decode_steps_out (host, or NULL) the
  * decode steps run.
  *
- * Scheduling: min(seqs_in_flight snapped to whole groups, n_prompts * G)
- * slots hold groups in prompt order.  Every refill_interval decode steps the
- * host reads the slots' ended flags; a range whose G completions have all
- * ended is given the next prompt's group, which is prefilled and draws its
- * token 0 there.  The call returns when every group has been admitted and has
- * ended.  Ended completions keep their slot until their whole group ends
- * (their rows are the padding that T_k excludes).  Errors: EINVAL (bad
- * argument, or a stop id outside [0, vocab), reported by rollout_sync),
- * ENOMEM, EDEVICE.
+ * Scheduling: every refill_interval decode steps the host reads the slots'
+ * ended flags and refills, in slot order, in completion order.
+ *  - whole_groups = 1: min(seqs_in_flight snapped to whole groups (section
+ *    4.3), n_prompts * G) slots in ranges of G; a range whose G completions
+ *    have all ended takes the next prompt's group (prefilled there, token 0
+ *    drawn from its logits).
+ *  - whole_groups = 0: min(seqs_in_flight, context rows - 1, n_prompts * G)
+ *    slots; a slot whose completion has ended takes the next completion.  A
+ *    group's prompt is prefilled once, when its first completion is admitted,
+ *    into a prompt record of KV blocks shared by its members (at most slots + 1
+ *    records are alive); every member's token 0 is drawn then.  Needs
+ *    (slots + 1) * ceil(prompt / block) + slots * (blocks from the last full
+ *    prompt block to the end) KV blocks; fewer slots are used if the pool is
+ *    smaller.
+ * The call returns when every completion has been admitted and has ended.
+ * Ended completions keep running in their slot until it is refilled (their
+ * rows are the padding that T_k excludes).  Errors: EINVAL (bad argument, or
+ * a stop id outside [0, vocab), reported by rollout_sync), ENOMEM, EDEVICE.
  */
 rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts,
                                     int32_t prompt_len, int32_t group_size, int32_t seqs_in_flight,
                                     int32_t max_new_tokens, float temperature, float top_p,
                                     const float* d_uniforms, const int32_t* d_stop_ids, int32_t n_stop,
-                                    int32_t refill_interval, int32_t* d_tokens_out, int32_t* d_lengths_out,
-                                    int32_t* d_group_step_out, int32_t* h_decode_steps_out);
+                                    int32_t refill_interval, int32_t whole_groups, int32_t* d_tokens_out,
+                                    int32_t* d_lengths_out, int32_t* d_admit_step_out,
+                                    int32_t* h_decode_steps_out);
 
 /*
  * Length-target reward of section 5 (its formula is not given; reading:

@@ -97,7 +97,7 @@ def _load():
         "rollout_last_error": ([vp], ctypes.c_char_p),
         "rollout_export_weight": ([vp, i32, vp], i32),
         "rollout_profile_decode_step": ([vp, vp, vp, ctypes.POINTER(StepProfile)], i32),
-        "rollout_generate_eos": ([vp, vp, i32, i32, i32, i32, i32, f32, f32, vp, vp, i32, i32, vp, vp, vp,
+        "rollout_generate_eos": ([vp, vp, i32, i32, i32, i32, i32, f32, f32, vp, vp, i32, i32, i32, vp, vp, vp,
                                   ctypes.POINTER(i32)], i32),
         "rollout_length_rewards": ([vp, i32, i32, vp, vp, vp], i32),
         "occ_rolling_mean": ([vp, ctypes.c_int64, f64, f64, vp], i32),
@@ -175,13 +175,14 @@ def rollout_generate(ctx, prompts, n_prompts: int, prompt_len: int, group_size: 
 
 def rollout_generate_eos(ctx, prompts, n_prompts: int, prompt_len: int, group_size: int, seqs_in_flight: int,
                          max_new_tokens: int, temperature: float, top_p: float, uniforms, stop_ids, n_stop: int,
-                         refill_interval: int, tokens_out, lengths_out, group_step_out=None) -> int:
+                         refill_interval: int, whole_groups: int, tokens_out, lengths_out,
+                         admit_step_out=None) -> int:
     """Returns the number of decode steps run."""
     steps = ctypes.c_int32(0)
     _check(lib.rollout_generate_eos(ctx, _ptr(prompts), n_prompts, prompt_len, group_size, seqs_in_flight,
                                     max_new_tokens, temperature, top_p, _ptr(uniforms), _ptr(stop_ids), n_stop,
-                                    refill_interval, _ptr(tokens_out), _ptr(lengths_out), _ptr(group_step_out),
-                                    ctypes.byref(steps)), ctx)
+                                    refill_interval, whole_groups, _ptr(tokens_out), _ptr(lengths_out),
+                                    _ptr(admit_step_out), ctypes.byref(steps)), ctx)
     return steps.value
 
 

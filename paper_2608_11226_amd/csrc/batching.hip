@@ -1,4 +1,5 @@
-// Stop-token termination and continuous batching of whole groups (device side).
+// Stop-token termination and continuous batching (device side): slots refilled
+// with whole groups, or with single completions.
 //
 // The paper's controller counts T_k, the non-padding tokens a generation batch
 // yields (section 4.5, eq. 4), and its runs reward closeness to a 128-token
@@ -10,8 +11,9 @@
 // k_cb_commit then files each live slot's draw under its completion, ends it
 // on a stop token or at max_new_tokens, and stages the next uniform.  Ended
 // slots keep running with their last token until the host refills their
-// group's range; their context length stops advancing, so their cache writes
-// stay inside the blocks their completion owned.
+// group's range (or, in single-completion refill, their slot); their context
+// length stops advancing, so their cache writes stay inside the blocks their
+// slot owns.
 #include "internal.h"
 
 namespace rollout {
@@ -83,6 +85,36 @@ __global__ void k_cb_commit(int r0, int r1, int N, const int32_t* __restrict__ d
   }
 }
 
+// single-completion refill: block-table row `row` = the prompt record's shared blocks (rec .. rec + n_shared),
+// then either the record's copy of the partial last prompt block (prefill row, own == -1) or the slot's own
+// blocks (own .. own + n_own); the rest -1
+__global__ void k_seq_table(int32_t* __restrict__ tables, int max_blocks, int row, int rec, int n_shared,
+                            int has_partial, int own, int n_own) {
+  int32_t* t = tables + (size_t)row * max_blocks;
+  for (int j = threadIdx.x; j < max_blocks; j += blockDim.x) {
+    int v = -1;
+    if (j < n_shared) v = rec + j;
+    else if (own < 0) v = (has_partial && j == n_shared) ? rec + n_shared : -1;
+    else if (j - n_shared < n_own) v = own + (j - n_shared);
+    t[j] = v;
+  }
+}
+
+// slot r starts completion s at context P with the token 0 its group's prefill drew (tokens_out[s][0]);
+// the rest of the completion's output row is padded
+__global__ void k_seq_admit(int r, int s, int P, int N, int32_t* __restrict__ seq, int32_t* __restrict__ col,
+                            int32_t* __restrict__ done, int32_t* __restrict__ draw, int32_t* __restrict__ ctx_len,
+                            int32_t* __restrict__ tokens_out) {
+  for (int i = 1 + threadIdx.x; i < N; i += blockDim.x) tokens_out[(size_t)s * N + i] = -1;
+  if (threadIdx.x == 0) {
+    seq[r] = s;
+    col[r] = 0;
+    done[r] = 0;
+    ctx_len[r] = P;
+    draw[r] = tokens_out[(size_t)s * N];
+  }
+}
+
 // rewards[i] = 1 - min(1, |L_i - target| / target); total[0] = sum of L_i (one workgroup)
 __global__ __launch_bounds__(256) void k_length_rewards(const int32_t* __restrict__ lengths, int n, int target,
                                                         float* __restrict__ rewards,
@@ -130,6 +162,20 @@ hipError_t launch_cb_commit(hipStream_t s, const CbState& cb, int r0, int r1, in
   if (r1 <= r0) return hipSuccess;
   hipLaunchKernelGGL(k_cb_commit, dim3((r1 - r0 + 255) / 256), dim3(256), 0, s, r0, r1, N, cb.draw, stop, u, cb.seq,
                      cb.col, cb.done, ctx_len, cb.u_slot, tokens_out, lengths, advance ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_seq_table(hipStream_t s, int32_t* tables, int max_blocks, int row, int rec, int n_shared,
+                            bool has_partial, int own, int n_own) {
+  hipLaunchKernelGGL(k_seq_table, dim3(1), dim3(256), 0, s, tables, max_blocks, row, rec, n_shared, has_partial ? 1 : 0,
+                     own, n_own);
+  return hipGetLastError();
+}
+
+hipError_t launch_seq_admit(hipStream_t s, const CbState& cb, int r, int seq_id, int P, int N, int32_t* ctx_len,
+                            int32_t* tokens_out) {
+  hipLaunchKernelGGL(k_seq_admit, dim3(1), dim3(256), 0, s, r, seq_id, P, N, cb.seq, cb.col, cb.done, cb.draw, ctx_len,
+                     tokens_out);
   return hipGetLastError();
 }
 

@@ -139,6 +139,10 @@ hipError_t launch_cb_commit(hipStream_t s, const CbState& cb, int r0, int r1, in
                             const float* u, int32_t* ctx_len, int32_t* tokens_out, int32_t* lengths, bool advance);
 hipError_t launch_length_rewards(hipStream_t s, const int32_t* lengths, int n, int target, float* rewards,
                                  long long* total);
+hipError_t launch_seq_table(hipStream_t s, int32_t* tables, int max_blocks, int row, int rec, int n_shared,
+                            bool has_partial, int own, int n_own);
+hipError_t launch_seq_admit(hipStream_t s, const CbState& cb, int r, int seq_id, int P, int N, int32_t* ctx_len,
+                            int32_t* tokens_out);
 hipError_t launch_set_cols(hipStream_t s, int32_t* cols, int c0, int c1);
 // Sampler scratch: stored e values of S rows plus per-chunk statistics.
 size_t sample_scratch_bytes(int S, int V);

@@ -236,6 +236,7 @@ struct rollout_ctx {
 
   // current wave
   bool wave = false;
+  bool seq_refill = false;  // the slots hold single completions of different groups (no shared-prefix attention)
   int S = 0, P = 0, G = 0, cur_len = 0, n_prompts = 0;
 
   Prof prof;
@@ -365,7 +366,7 @@ bool use_shared_prefix(const rollout_ctx* c, int M, const RowMap& rm) {
   const char* v = std::getenv("ROLLOUT_SHARED_PREFIX");
   const int mode = v ? std::atoi(v) : 1;
   const int p_shared = c->P / c->D.blk * c->D.blk;
-  if (mode == 0 || !c->wave || c->G < 2 || p_shared < c->D.blk || M % c->G || rm.seq0 % c->G) return false;
+  if (mode == 0 || !c->wave || c->seq_refill || c->G < 2 || p_shared < c->D.blk || M % c->G || rm.seq0 % c->G) return false;
   return mode == 2 || (int64_t)c->G * p_shared >= 8192;
 }
 
@@ -473,6 +474,7 @@ rollout_status upload_wave(rollout_ctx* c, int n_prompts, int P, int G) {
   HIP_TRY(c, hipMemcpyAsync(c->at(Lo.tables), t, (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipMemcpyHostToDevice,
                             c->stream), "block table upload");
   c->wave = true;
+  c->seq_refill = false;
   c->S = S;
   c->P = P;
   c->G = G;
@@ -481,10 +483,11 @@ rollout_status upload_wave(rollout_ctx* c, int n_prompts, int P, int G) {
   return ROLLOUT_OK;
 }
 
-// Prefill n_prompts prompts whose groups occupy the slots from row0 on (G rows each, block tables already
-// in place); the last position's logits, replicated per sequence, go to d_logits [n_prompts * G, V].
-rollout_status prefill_rows(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G, int row0,
-                            float* d_logits) {
+// Prefill n_prompts prompts.  Prompt i writes its K/V through the block-table rows row0 + i * G_kv ..
+// + G_kv - 1 (tables already in place; the partial last prompt block goes to each of them); the last
+// position's logits, replicated G_out times, go to d_logits [n_prompts * G_out, V].
+rollout_status prefill_rows(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G_kv, int G_out,
+                            int row0, float* d_logits) {
   const Dims& D = c->D;
   const Layout& Lo = c->Lo;
   const int per_chunk = std::max(1, Lo.T_chunk / P);
@@ -496,12 +499,13 @@ rollout_status prefill_rows(rollout_ctx* c, const int32_t* d_prompts, int n_prom
       HIP_TRY(c, launch_embed(c->stream, D.dtype, c->at(Lo.embed), d_prompts + (size_t)p0 * P, 1, nullptr, M, D.d, D.V,
                               c->at<float>(Lo.x), c->at<int32_t>(Lo.err)), "embed");
     }
-    RowMap rm{nullptr, P, G, row0 + p0 * G};
+    RowMap rm{nullptr, P, G_kv, row0 + p0 * G_kv};
     rollout_status r = forward_layers(c, M, rm, P, (double)np * P * (P + 1) / 2.0);
     if (r) return r;
-    HIP_TRY(c, launch_gather_rows(c->stream, D.dtype, c->at(Lo.a), D.d, P, G, np, c->at(Lo.a_last)), "gather");
+    HIP_TRY(c, launch_gather_rows(c->stream, D.dtype, c->at(Lo.a), D.d, P, G_out, np, c->at(Lo.a_last)), "gather");
     int s;
-    r = gemm(c, c->at(Lo.a_last), c->at(Lo.lm_head), d_logits + (size_t)p0 * G * D.V, np * G, D.V, D.d, 1, &s);
+    r = gemm(c, c->at(Lo.a_last), c->at(Lo.lm_head), d_logits + (size_t)p0 * G_out * D.V, np * G_out, D.V, D.d, 1,
+             &s);
     if (r) return r;
   }
   return ROLLOUT_OK;
@@ -510,7 +514,7 @@ rollout_status prefill_rows(rollout_ctx* c, const int32_t* d_prompts, int n_prom
 rollout_status do_prefill(rollout_ctx* c, const int32_t* d_prompts, int n_prompts, int P, int G, float* d_logits) {
   rollout_status r = upload_wave(c, n_prompts, P, G);
   if (r) return r;
-  return prefill_rows(c, d_prompts, n_prompts, P, G, 0, d_logits);
+  return prefill_rows(c, d_prompts, n_prompts, P, G, G, 0, d_logits);
 }
 
 // Enqueue one decode step of the current wave (no host-side state change).
@@ -832,12 +836,13 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
                                     int32_t prompt_len, int32_t group_size, int32_t seqs_in_flight,
                                     int32_t max_new_tokens, float temperature, float top_p, const float* d_uniforms,
                                     const int32_t* d_stop_ids, int32_t n_stop, int32_t refill_interval,
-                                    int32_t* d_tokens_out, int32_t* d_lengths_out, int32_t* d_group_step_out,
-                                    int32_t* h_decode_steps_out) {
+                                    int32_t whole_groups, int32_t* d_tokens_out, int32_t* d_lengths_out,
+                                    int32_t* d_admit_step_out, int32_t* h_decode_steps_out) {
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   if (!d_prompts || !d_uniforms || !d_tokens_out || !d_lengths_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
   if (n_stop < 0 || (n_stop > 0 && !d_stop_ids)) return fail(ctx, ROLLOUT_EINVAL, "n_stop < 0 or stop ids NULL");
   if (refill_interval < 1) return fail(ctx, ROLLOUT_EINVAL, "refill_interval must be >= 1");
+  if (whole_groups != 0 && whole_groups != 1) return fail(ctx, ROLLOUT_EINVAL, "whole_groups must be 0 or 1");
   if (n_prompts < 1 || group_size < 1 || seqs_in_flight < 1)
     return fail(ctx, ROLLOUT_EINVAL, "n_prompts, group_size and seqs_in_flight must be >= 1");
   if (prompt_len < 1 || prompt_len > ctx->cfg.max_prompt_len)
@@ -849,41 +854,105 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
   const Dims& D = ctx->D;
   const Layout& Lo = ctx->Lo;
   const int G = group_size, P = prompt_len, N = max_new_tokens;
-  // slots: whole groups, within the context's rows and the KV pool, no more ranges than prompts
-  int S = std::min<int64_t>(seqs_in_flight, Lo.S) / G * G;
-  const int ctxlen = P + ctx->cfg.max_new_tokens;
-  while (S >= G && blocks_needed(S / G, G, P, ctxlen, D.blk) > ctx->n_blocks) S -= G;
-  if (S < G) return fail(ctx, ROLLOUT_ENOMEM, "one group does not fit in the context");
-  const int ranges = std::min(S / G, (int)n_prompts);
-  S = ranges * G;
-  // every range keeps its block-table rows for the whole call; a refilled range reuses them
+  const int n_seq = n_prompts * G;
+  // KV blocks: a group's full prompt blocks are shared; positions from there on belong to a slot
+  const int n_shared = P / D.blk;
+  const bool partial = P % D.blk != 0;
+  const int n_own = (P + N + D.blk - 1) / D.blk - n_shared;
+  const int n_rec = n_shared + (partial ? 1 : 0);  // a prompt record: shared blocks + its partial block
+  int S;
+  if (whole_groups) {
+    // whole groups, within the context's rows and the KV pool, no more ranges than prompts
+    S = std::min<int64_t>(seqs_in_flight, Lo.S) / G * G;
+    const int ctxlen = P + ctx->cfg.max_new_tokens;
+    while (S >= G && blocks_needed(S / G, G, P, ctxlen, D.blk) > ctx->n_blocks) S -= G;
+    if (S < G) return fail(ctx, ROLLOUT_ENOMEM, "one group does not fit in the context");
+    S = std::min(S / G, (int)n_prompts) * G;
+  } else {
+    // single completions: one block-table row beyond the slots serves the prefills; up to S + 1 prompt
+    // records are alive at once (a group per occupied slot, plus the one being admitted)
+    S = std::min<int64_t>(std::min<int64_t>(seqs_in_flight, Lo.S - 1), n_seq);
+    while (S >= 1 && (int64_t)(S + 1) * n_rec + (int64_t)S * n_own > ctx->n_blocks) --S;
+    if (S < 1) return fail(ctx, ROLLOUT_ENOMEM, "one completion does not fit in the context");
+  }
   ctx->wave = false;
-  rollout_status r = upload_wave(ctx, ranges, P, G);
-  if (r) return r;
+  int32_t* tables = ctx->at<int32_t>(Lo.tables);
+  int32_t* ctx_len = ctx->at<int32_t>(Lo.ctx_len);
+  if (whole_groups) {
+    // every range keeps its block-table rows for the whole call; a refilled range reuses them
+    rollout_status r = upload_wave(ctx, S / G, P, G);
+    if (r) return r;
+  } else {
+    HIP_TRY(ctx, hipStreamSynchronize(ctx->stream), "stream sync");
+    ctx->wave = true;
+    ctx->seq_refill = true;
+    ctx->S = S;
+    ctx->P = P;
+    ctx->G = G;
+    ctx->n_prompts = n_prompts;
+    ctx->cur_len = P;
+  }
   int32_t* base = ctx->at<int32_t>(Lo.cb);
   const CbState cb{base, base + S, base + 2 * S, base + 3 * S, reinterpret_cast<float*>(base + 4 * S)};
   uint32_t* stop = n_stop > 0 ? ctx->at<uint32_t>(Lo.stopmap) : nullptr;
   if (stop) HIP_TRY(ctx, launch_stop_bitmap(ctx->stream, stop, D.V, d_stop_ids, n_stop, ctx->at<int32_t>(Lo.err)), "stop set");
   HIP_TRY(ctx, launch_cb_reset(ctx->stream, S, cb), "slot reset");
   float* logits = ctx->at<float>(Lo.logits);
-  int32_t* ctx_len = ctx->at<int32_t>(Lo.ctx_len);
   void* samp = ctx->at(Lo.samp);
-  std::vector<int> range_group(ranges, -1);
-  std::vector<int32_t> admit_step(n_prompts, -1);
-  int next = 0;
-  // a range takes the next prompt's group: reset its slots, prefill, draw token 0 from the prefill logits
-  auto admit = [&](int k, int boundary) -> rollout_status {
-    const int p = next++;
+  std::vector<int32_t> admit_step(n_seq, -1);
+  // host view of the slots: completion per slot (-1 none); whole groups use slot ranges of G
+  std::vector<int> slot_seq(S, -1);
+  int next = 0;  // next completion to admit, in order s = p * G + g
+  // --- whole groups: a range takes the next prompt's group: reset its slots, prefill, draw token 0
+  auto admit_group = [&](int k, int boundary) -> rollout_status {
+    const int p = next / G;
     const int r0 = k * G, seq0 = p * G;
-    admit_step[p] = boundary;
-    range_group[k] = p;
+    for (int g = 0; g < G; ++g) {
+      admit_step[seq0 + g] = boundary;
+      slot_seq[r0 + g] = seq0 + g;
+    }
+    next += G;
     HIP_TRY(ctx, launch_cb_admit(ctx->stream, cb, r0, G, seq0, P, N, ctx_len, d_tokens_out), "admit");
-    rollout_status rr = prefill_rows(ctx, d_prompts + (size_t)p * P, 1, P, G, r0, logits);
+    rollout_status rr = prefill_rows(ctx, d_prompts + (size_t)p * P, 1, P, G, G, r0, logits);
     if (rr) return rr;
     HIP_TRY(ctx, launch_sample(ctx->stream, logits, G, D.V, temperature, top_p, d_uniforms + (size_t)seq0 * N, N,
                                nullptr, cb.draw + r0, 1, samp), "sample");
     HIP_TRY(ctx, launch_cb_commit(ctx->stream, cb, r0, r0 + G, N, stop, d_uniforms, ctx_len, d_tokens_out,
                                   d_lengths_out, false), "commit");
+    return ROLLOUT_OK;
+  };
+  // --- single completions: prompt records [0, S], own blocks of slot r after them
+  std::vector<int> rec_free, rec_of(n_prompts, -1), ended_of(n_prompts, 0);
+  for (int k = S; k >= 0; --k) rec_free.push_back(k);
+  const int own0 = (S + 1) * n_rec;
+  auto admit_seq = [&](int r, int boundary) -> rollout_status {
+    const int s = next++, p = s / G, g = s % G;
+    if (g == 0) {  // the group's first completion: prefill its prompt into a free record, draw every token 0
+      if (rec_free.empty()) return fail(ctx, ROLLOUT_EINVAL, "internal: no free prompt record");
+      const int k = rec_free.back();
+      rec_free.pop_back();
+      rec_of[p] = k;
+      HIP_TRY(ctx, launch_seq_table(ctx->stream, tables, Lo.max_blocks, S, k * n_rec, n_shared, partial, -1, 0),
+              "prefill table");
+      rollout_status rr = prefill_rows(ctx, d_prompts + (size_t)p * P, 1, P, 1, G, S, logits);
+      if (rr) return rr;
+      HIP_TRY(ctx, launch_sample(ctx->stream, logits, G, D.V, temperature, top_p, d_uniforms + (size_t)p * G * N, N,
+                                 nullptr, d_tokens_out + (size_t)p * G * N, N, samp), "sample");
+    }
+    const int k = rec_of[p];
+    HIP_TRY(ctx, launch_seq_table(ctx->stream, tables, Lo.max_blocks, r, k * n_rec, n_shared, partial, own0 + r * n_own,
+                                  n_own), "slot table");
+    if (partial) {  // the slot's first own block starts as the record's copy of the partial prompt block
+      char* kvp = ctx->arena + Lo.work_end;
+      HIP_TRY(ctx, hipMemcpyAsync(kvp + (size_t)(own0 + r * n_own) * Lo.kv_block_bytes,
+                                  kvp + (size_t)(k * n_rec + n_shared) * Lo.kv_block_bytes, Lo.kv_block_bytes,
+                                  hipMemcpyDeviceToDevice, ctx->stream), "partial block");
+    }
+    HIP_TRY(ctx, launch_seq_admit(ctx->stream, cb, r, s, P, N, ctx_len, d_tokens_out), "admit");
+    HIP_TRY(ctx, launch_cb_commit(ctx->stream, cb, r, r + 1, N, stop, d_uniforms, ctx_len, d_tokens_out, d_lengths_out,
+                                  false), "commit");
+    admit_step[s] = boundary;
+    slot_seq[r] = s;
     return ROLLOUT_OK;
   };
   // one decode step over all slots: feed each slot's last draw, draw with its staged uniform, file the draws
@@ -896,14 +965,21 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
                                   true), "commit");
     return ROLLOUT_OK;
   };
-  for (int k = 0; k < ranges; ++k)
-    if ((r = admit(k, 0))) return r;
+  rollout_status r = ROLLOUT_OK;
+  if (whole_groups) {
+    for (int k = 0; k < S / G && !r; ++k) r = admit_group(k, 0);
+  } else {
+    for (int i = 0; i < S && !r; ++i) r = admit_seq(i, 0);
+  }
+  if (r) return r;
   hipGraphExec_t exec = nullptr;
   auto finish = [&](rollout_status st) {
     if (exec) {
       hipStreamSynchronize(ctx->stream);
       hipGraphExecDestroy(exec);
+      exec = nullptr;
     }
+    ctx->wave = false;  // the slots' state is not a wave that rollout_decode_step may continue
     return st;
   };
   if (!ctx->prof.on) {
@@ -913,17 +989,17 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
     hipError_t ce = hipStreamEndCapture(ctx->stream, &graph);
     if (r) {
       if (graph) hipGraphDestroy(graph);
-      return r;
+      return finish(r);
     }
-    if (ce != hipSuccess) return hip_fail(ctx, ce, "end capture");
+    if (ce != hipSuccess) return finish(hip_fail(ctx, ce, "end capture"));
     hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
     hipGraphDestroy(graph);
-    if (ie != hipSuccess) return hip_fail(ctx, ie, "graph instantiate");
+    if (ie != hipSuccess) return finish(hip_fail(ctx, ie, "graph instantiate"));
   }
   int steps = 0;
   auto live = [&]() {
-    for (int k = 0; k < ranges; ++k)
-      if (range_group[k] >= 0) return true;
+    for (int i = 0; i < S; ++i)
+      if (slot_seq[i] >= 0) return true;
     return false;
   };
   while (live()) {
@@ -939,20 +1015,29 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
     hipError_t ce = hipMemcpyAsync(ctx->h_done, cb.done, (size_t)S * 4, hipMemcpyDeviceToHost, ctx->stream);
     if (ce == hipSuccess) ce = hipStreamSynchronize(ctx->stream);
     if (ce != hipSuccess) return finish(hip_fail(ctx, ce, "ended flags read"));
-    for (int k = 0; k < ranges; ++k) {
-      if (range_group[k] < 0) continue;
-      bool ended = true;
-      for (int g = 0; g < G; ++g) ended = ended && ctx->h_done[k * G + g] != 0;
-      if (!ended) continue;
-      range_group[k] = -1;
-      if (next < n_prompts && (r = admit(k, steps))) return finish(r);
+    if (whole_groups) {
+      for (int k = 0; k < S / G; ++k) {
+        if (slot_seq[k * G] < 0) continue;
+        bool ended = true;
+        for (int g = 0; g < G; ++g) ended = ended && ctx->h_done[k * G + g] != 0;
+        if (!ended) continue;
+        for (int g = 0; g < G; ++g) slot_seq[k * G + g] = -1;
+        if (next < n_seq && (r = admit_group(k, steps))) return finish(r);
+      }
+    } else {
+      for (int i = 0; i < S; ++i) {
+        const int s = slot_seq[i];
+        if (s < 0 || !ctx->h_done[i]) continue;
+        slot_seq[i] = -1;
+        if (++ended_of[s / G] == G) rec_free.push_back(rec_of[s / G]);
+        if (next < n_seq && (r = admit_seq(i, steps))) return finish(r);
+      }
     }
   }
   r = finish(ROLLOUT_OK);
-  exec = nullptr;
-  if (d_group_step_out)
-    HIP_TRY(ctx, hipMemcpy(d_group_step_out, admit_step.data(), (size_t)n_prompts * 4, hipMemcpyHostToDevice),
-            "group steps");
+  if (d_admit_step_out)
+    HIP_TRY(ctx, hipMemcpy(d_admit_step_out, admit_step.data(), (size_t)n_seq * 4, hipMemcpyHostToDevice),
+            "admission steps");
   if (h_decode_steps_out) *h_decode_steps_out = steps;
   return r;
 }

@@ -7,7 +7,7 @@ import paper_2608_11226_amd as R
 import workload as W
 from gpu_helpers import guarded_token_compare, log, shape_of, to_dev
 from oracle import OracleModel, rollout
-from oracle.batching import continuous_schedule, length_target_reward, rollout_eos
+from oracle.batching import continuous_schedule, length_target_reward, rollout_eos, sequence_schedule
 
 pytestmark = pytest.mark.gpu
 
@@ -16,19 +16,27 @@ torch = pytest.importorskip("torch")
 SMALL_BF16 = (2, 256, 8, 2, 64, 512, 2048, 1e6)
 
 
-def _run_eos(eng, prompts, G, slots, N, T, top_p, u, stop, refill):
+def _run_eos(eng, prompts, G, slots, N, T, top_p, u, stop, refill, whole_groups=1):
     n_prompts, P = prompts.shape
     S = n_prompts * G
     dev = "cuda:0"
     tokens = torch.full((S, N), -7, dtype=torch.int32, device=dev)
     lengths = torch.full((S,), -7, dtype=torch.int32, device=dev)
-    gstep = torch.full((n_prompts,), -7, dtype=torch.int32, device=dev)
+    admit = torch.full((S,), -7, dtype=torch.int32, device=dev)
     stop_t = to_dev(np.asarray(stop, dtype=np.int32), torch) if len(stop) else torch.zeros(1, dtype=torch.int32,
                                                                                             device=dev)
     steps = R.rollout_generate_eos(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, slots, N, T, top_p,
-                                   to_dev(u, torch), stop_t, len(stop), refill, tokens, lengths, gstep)
+                                   to_dev(u, torch), stop_t, len(stop), refill, whole_groups, tokens, lengths, admit)
     eng.synchronize()
-    return tokens.cpu().numpy(), lengths.cpu().numpy(), gstep.cpu().numpy(), steps
+    return tokens.cpu().numpy(), lengths.cpu().numpy(), admit.cpu().numpy(), steps
+
+
+def _expected_schedule(L, G, slots, refill, whole_groups):
+    if whole_groups:
+        sch = continuous_schedule(L, G, slots // G, refill)
+        return np.repeat(sch["admit"], G), sch["steps"]
+    sch = sequence_schedule(L, slots, refill)
+    return sch["admit"], sch["steps"]
 
 
 def _check_structure(tokens, lengths, stop, N, V):
@@ -44,11 +52,13 @@ def _check_structure(tokens, lengths, stop, N, V):
         assert (hits and hits[0] == L - 1) or (not hits and L == N), f"completion {s}: stop rule"
 
 
+@pytest.mark.parametrize("whole_groups", [1, 0])
 @pytest.mark.parametrize("T,top_p,refill", [(1.0, 1.0, 1), (0.8, 0.9, 3), (0.0, 1.0, 2)])
-def test_tiny_fp32_eos_matches_oracle(T, top_p, refill):
+def test_tiny_fp32_eos_matches_oracle(T, top_p, refill, whole_groups):
     G, n_prompts, P, N, slots = 4, 5, 12, 16, 8
-    log(f"tiny fp32 eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill}, T={T} top_p={top_p}")
-    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, slots)
+    log(f"tiny fp32 eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill} "
+        f"({'whole groups' if whole_groups else 'single completions'}), T={T} top_p={top_p}")
+    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, 2 * slots)  # room for the prompt records of single refill
     eng = R.Engine(cfg, group_size=G)
     model = OracleModel(shape_of(cfg), mode="fp32")
     prompts = W.prompts(n_prompts, P, cfg.vocab, seed=51)
@@ -57,7 +67,7 @@ def test_tiny_fp32_eos_matches_oracle(T, top_p, refill):
     # stop tokens taken from the draws themselves so that the completions end at different lengths
     stop = sorted({int(plain[0, 2]), int(plain[5, 6]), int(plain[9, 0]), int(plain[14, 11])})
     ref = rollout_eos(model, prompts, G, N, T, top_p, u, stop)
-    tok, L, gstep, steps = _run_eos(eng, prompts, G, slots, N, T, top_p, u, stop, refill)
+    tok, L, admit, steps = _run_eos(eng, prompts, G, slots, N, T, top_p, u, stop, refill, whole_groups)
     _check_structure(tok, L, stop, N, cfg.vocab)
     compared, skipped = guarded_token_compare(tok, np.where(ref["tokens"] < 0, -1, ref["tokens"]), ref["margins"])
     log(f"  lengths {L.tolist()}; compared {compared} tokens, skipped {skipped} after near-ties")
@@ -66,21 +76,22 @@ def test_tiny_fp32_eos_matches_oracle(T, top_p, refill):
         assert L[s] == ref["lengths"][s], f"completion {s}: length {L[s]} oracle {ref['lengths'][s]}"
     assert compared >= 60 and len(exact) >= n_prompts * G // 2
     # the schedule follows the refill rule for the lengths the device produced
-    sch = continuous_schedule(L, G, slots // G, refill)
-    assert list(gstep) == list(sch["admit"]) and steps == sch["steps"], (gstep, sch)
-    assert len(set(gstep.tolist())) > 1, "no refill happened"
+    want_admit, want_steps = _expected_schedule(L, G, slots, refill, whole_groups)
+    assert list(admit) == list(want_admit) and steps == want_steps, (admit, want_admit, steps, want_steps)
+    assert len(set(admit.tolist())) > 1, "no refill happened"
     eng.close()
 
 
-def test_tiny_fp32_eos_without_stop_set_equals_generate():
-    G, n_prompts, P, N = 2, 4, 16, 12
-    log("tiny fp32 eos with an empty stop set against rollout_generate")
-    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, 8)
+@pytest.mark.parametrize("whole_groups,P", [(1, 16), (0, 16), (0, 20)])
+def test_tiny_fp32_eos_without_stop_set_equals_generate(whole_groups, P):
+    G, n_prompts, N = 2, 4, 12
+    log(f"tiny fp32 eos with an empty stop set against rollout_generate, whole_groups={whole_groups} P={P}")
+    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, 32)  # a KV pool with room for 8 slots and 9 prompt records
     eng = R.Engine(cfg, group_size=G)
     prompts = W.prompts(n_prompts, P, cfg.vocab, seed=21)
     u = W.uniforms(n_prompts * G, N, seed=22)
-    tok, L, gstep, steps = _run_eos(eng, prompts, G, 8, N, 0.8, 0.9, u, [], 4)
-    assert np.all(L == N) and list(gstep) == [0] * n_prompts and steps == 12
+    tok, L, admit, steps = _run_eos(eng, prompts, G, 8, N, 0.8, 0.9, u, [], 4, whole_groups)
+    assert np.all(L == N) and list(admit) == [0] * (n_prompts * G) and steps == 12
     out = torch.full((n_prompts * G, N), -1, dtype=torch.int32, device="cuda:0")
     R.rollout_generate(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, 8, N, 0.8, 0.9, to_dev(u, torch), out)
     eng.synchronize()
@@ -88,28 +99,46 @@ def test_tiny_fp32_eos_without_stop_set_equals_generate():
     eng.close()
 
 
-@pytest.mark.parametrize("refill,slots", [(1, 8), (4, 16), (2, 4)])
-def test_bf16_eos_schedule_and_stop_rule(refill, slots):
-    G, n_prompts, P, N = 4, 7, 40, 24
-    log(f"bf16 small GQA eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill}")
-    cfg = R.model_config(SMALL_BF16, R.DTYPE_BF16, P, N, slots)
+@pytest.mark.parametrize("refill,slots,whole_groups,P", [(1, 8, 1, 40), (4, 16, 1, 40), (2, 4, 1, 40),
+                                                         (1, 8, 0, 40), (3, 12, 0, 32), (2, 5, 0, 40)])
+def test_bf16_eos_schedule_and_stop_rule(refill, slots, whole_groups, P):
+    G, n_prompts, N = 4, 7, 24
+    log(f"bf16 small GQA eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill}, "
+        f"whole_groups={whole_groups}, P={P}")
+    cfg = R.model_config(SMALL_BF16, R.DTYPE_BF16, P, N, 2 * slots + G)
     eng = R.Engine(cfg, group_size=G)
     prompts = W.prompts(n_prompts, P, cfg.vocab, seed=61)
     u = W.uniforms(n_prompts * G, N, seed=62)
     stop = list(range(0, cfg.vocab, 16))  # 1 in 16 ids: random-init completions end after ~16 tokens
-    tok, L, gstep, steps = _run_eos(eng, prompts, G, slots, N, 1.0, 1.0, u, stop, refill)
+    tok, L, admit, steps = _run_eos(eng, prompts, G, slots, N, 1.0, 1.0, u, stop, refill, whole_groups)
     _check_structure(tok, L, stop, N, cfg.vocab)
     log(f"  lengths mean {L.mean():.1f} min {L.min()} max {L.max()}; {steps} decode steps")
-    sch = continuous_schedule(L, G, min(slots // G, n_prompts), refill)
-    assert list(gstep) == list(sch["admit"]) and steps == sch["steps"]
+    eff_slots = min(slots, n_prompts * G) if not whole_groups else min(slots // G, n_prompts) * G
+    want_admit, want_steps = _expected_schedule(L, G, eff_slots, refill, whole_groups)
+    assert list(admit) == list(want_admit) and steps == want_steps
     assert L.min() < N and len(set(L.tolist())) > 3
     # token 0 of every completion is drawn from its prompt's prefill logits: the same as rollout_generate's
     out = torch.full((n_prompts * G, N), -1, dtype=torch.int32, device="cuda:0")
-    R.rollout_generate(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, slots, N, 1.0, 1.0, to_dev(u, torch), out)
+    R.rollout_generate(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, 8, N, 1.0, 1.0, to_dev(u, torch), out)
     eng.synchronize()
     same0 = float(np.mean(out.cpu().numpy()[:, 0] == tok[:, 0]))
     log(f"  token 0 agreement with rollout_generate: {same0:.2f}")
     assert same0 >= 0.9
+    eng.close()
+
+
+def test_single_refill_matches_whole_group_refill_tokens():
+    # the same completions, whichever slots and steps serve them
+    G, n_prompts, P, N = 2, 6, 20, 14
+    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, 16)
+    eng = R.Engine(cfg, group_size=G)
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=81)
+    u = W.uniforms(n_prompts * G, N, seed=82)
+    stop = list(range(0, cfg.vocab, 9))
+    a = _run_eos(eng, prompts, G, 4, N, 1.0, 1.0, u, stop, 2, 1)
+    b = _run_eos(eng, prompts, G, 5, N, 1.0, 1.0, u, stop, 3, 0)
+    log(f"  decode steps: whole groups {a[3]}, single completions {b[3]}")
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
     eng.close()
 
 
@@ -134,7 +163,7 @@ def test_bad_stop_id_is_reported():
     tokens = torch.empty((4, 4), dtype=torch.int32, device=dev)
     lengths = torch.empty(4, dtype=torch.int32, device=dev)
     stop = torch.tensor([3, cfg.vocab + 9], dtype=torch.int32, device=dev)
-    R.rollout_generate_eos(eng.ctx, to_dev(prompts, torch), 2, 8, 2, 4, 4, 1.0, 1.0, to_dev(u, torch), stop, 2, 1,
+    R.rollout_generate_eos(eng.ctx, to_dev(prompts, torch), 2, 8, 2, 4, 4, 1.0, 1.0, to_dev(u, torch), stop, 2, 1, 1,
                            tokens, lengths)
     with pytest.raises(R.RolloutError, match="outside"):
         eng.synchronize()
