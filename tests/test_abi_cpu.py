@@ -136,3 +136,14 @@ def test_validation_before_device_work():
     with pytest.raises(R.RolloutError) as e:
         R.rollout_init(cfg, 0x1001, 10**12)  # misaligned
     assert e.value.code == R.EINVAL
+
+
+def test_stop_token_entry_points_validate_before_device_work():
+    # rollout_generate_eos without a context, and the length reward's arguments
+    with pytest.raises(R.RolloutError) as e:
+        R.rollout_generate_eos(None, 0x1000, 2, 8, 2, 4, 4, 1.0, 1.0, 0x2000, 0x3000, 1, 1, 1, 0x4000, 0x5000)
+    assert e.value.code == R.EINVAL
+    for args in ((None, 4, 128, 0x2000), (0x1000, 4, 128, None), (0x1000, 0, 128, 0x2000), (0x1000, 4, 0, 0x2000)):
+        with pytest.raises(R.RolloutError) as e:
+            R.rollout_length_rewards(*args)
+        assert e.value.code == R.EINVAL
