@@ -75,9 +75,11 @@ constexpr int kTileMB = 8;            // 16-row activation blocks per workgroup
 constexpr int kTileWaves = 4;
 constexpr int kTileXPW = kTileMB / kTileWaves;  // activation fragments each wave stages per k-step
 
+// SWI: gate/up with SwiGLU applied to the output (one K split): h in the down projection's operand layout
+template <bool SWI>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W, float* __restrict__ out,
-                 int M, int N, int K, int kslice) {
+                 int M, int N, int K, int kslice, uint16_t* __restrict__ h) {
   __shared__ bf16x8_t xs[2][kTileMB][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -169,8 +171,15 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
 #pragma unroll
     for (int i = 0; i < kTileMB; ++i) {
       const int m = (mb0 + i) * 16 + (lane & 15);
-      if (m < M)
+      if (m >= M) continue;
+      if constexpr (SWI) {
+        // rows n, n+1 are (gate, up) of output f = n/2; rows n+2, n+3 of output f + 1
+        const float g0 = acc[j][i][0], u0 = acc[j][i][1], g1 = acc[j][i][2], u1 = acc[j][i][3];
+        const float h0 = g0 / (1.0f + expf(-g0)) * u0, h1 = g1 / (1.0f + expf(-g1)) * u1;
+        *reinterpret_cast<uint32_t*>(h + xoff(h, m, n >> 1, N >> 1, Mb)) = pack_bf16x2(h0, h1);
+      } else {
         *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
+      }
     }
   }
 }
@@ -451,7 +460,8 @@ int tile_groups(int M, int N) { return (tile_n_tiles(N) + 7) / 8 * 8 * tile_m_ti
 hipError_t launch_tile(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
                        int splits) {
   const dim3 grid(tile_groups(M, N), splits);
-  hipLaunchKernelGGL(k_gemm_tile, grid, dim3(64 * kTileWaves), 0, s, x, w, out, M, N, K, kslice_for(K, splits));
+  hipLaunchKernelGGL(k_gemm_tile<false>, grid, dim3(64 * kTileWaves), 0, s, x, w, out, M, N, K, kslice_for(K, splits),
+                     nullptr);
   return hipGetLastError();
 }
 
@@ -570,7 +580,13 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
 
 hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h) {
   if (M <= 0) return hipSuccess;
-  if (M > kSwigluMaxRows || M > kRingMaxRows || N % 16 || K % 32) return hipErrorInvalidValue;
+  if (N % 32 || K % 32) return hipErrorInvalidValue;
+  if (M > kRingMaxRows) {  // larger batches: the tile kernel with the same epilogue, one K split
+    const dim3 grid(tile_groups(M, N), 1);
+    hipLaunchKernelGGL(k_gemm_tile<true>, grid, dim3(64 * kTileWaves), 0, s, (const bf16x8_t*)X, (const bf16x8_t*)W,
+                       nullptr, M, N, K, kslice_for(K, 1), (uint16_t*)h);
+    return hipGetLastError();
+  }
   return launch_ring<4, true>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, 1, (uint16_t*)h);
 }
 

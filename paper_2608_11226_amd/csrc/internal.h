@@ -80,9 +80,10 @@ int gemm_splits(int dtype, int M, int N, int K, int max_splits);
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const void* W, float* out, int M,
                        int N, int K, int splits);
 
-// Decode gate/up projection with SwiGLU applied to its own output (bf16, one
-// K split, M <= kSwigluMaxRows): W holds gate row i at physical row 2i and up
-// row i at 2i + 1; h[m][i] = silu(gate) * up in the down projection's operand layout.
+// Gate/up projection with SwiGLU applied to its own output (bf16, one K split;
+// the ring kernel up to 64 rows, the tile kernel above): W holds gate row i at
+// physical row 2i and up row i at 2i + 1; h[m][i] = silu(gate) * up in the down
+// projection's operand layout.  int4 weights: the int4 ring, M <= kSwigluMaxRows.
 constexpr int kSwigluMaxRows = 64;
 hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M, int N, int K, void* h);
 // The same two GEMMs over an int4 weight matrix (M <= 64; K a multiple of 128; partial splits as above).

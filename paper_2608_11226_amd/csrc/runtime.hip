@@ -317,7 +317,7 @@ rollout_status gemm(rollout_ctx* c, const void* X, const void* W, float* out, in
   return ROLLOUT_OK;
 }
 
-// Decode gate/up GEMM with SwiGLU applied to its own output (bf16 or int4 weights, M <= kSwigluMaxRows).
+// Gate/up GEMM with SwiGLU applied to its own output (bf16 weights: any M; int4: M <= kSwigluMaxRows).
 rollout_status gemm_swiglu(rollout_ctx* c, const void* X, const void* W, int M, int N, int K, void* h) {
   const double eb = (double)elem_bytes(c->D.dtype);
   const double wb = c->D.wq4 ? (double)(q4_code_bytes(N, K) + q4_sz_bytes(N, K)) : (double)N * K * eb;
@@ -427,7 +427,8 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
       HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, part, s, M, D.d, x, c->at<float>(y.mlp_norm), D.eps, a),
               "residual norm");
     }
-    if (D.dtype == ROLLOUT_DTYPE_BF16 && M <= kSwigluMaxRows) {
+    // SwiGLU in the gate/up GEMM's epilogue; int4 weights only up to the int4 ring's rows
+    if (D.dtype == ROLLOUT_DTYPE_BF16 && (!D.wq4 || M <= kSwigluMaxRows)) {
       if ((r = gemm_swiglu(c, a, c->at(y.wgu), M, 2 * D.ff, D.d, h))) return r;
     } else {
       if ((r = proj(c, a, c->at(y.wgu), part, M, 2 * D.ff, D.d, &s))) return r;
