@@ -846,6 +846,8 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
   if (whole_groups != 0 && whole_groups != 1) return fail(ctx, ROLLOUT_EINVAL, "whole_groups must be 0 or 1");
   if (n_prompts < 1 || group_size < 1 || seqs_in_flight < 1)
     return fail(ctx, ROLLOUT_EINVAL, "n_prompts, group_size and seqs_in_flight must be >= 1");
+  if ((int64_t)n_prompts * group_size > INT32_MAX)
+    return fail(ctx, ROLLOUT_EINVAL, "n_prompts * group_size exceeds the int32 completion index");
   if (prompt_len < 1 || prompt_len > ctx->cfg.max_prompt_len)
     return fail(ctx, ROLLOUT_EINVAL, "prompt_len must be in [1, max_prompt_len]");
   if (max_new_tokens < 1 || max_new_tokens > ctx->cfg.max_new_tokens)
