@@ -554,11 +554,23 @@ hipError_t launch_gemm_swiglu_q4(hipStream_t s, const void* X, const void* W, in
 int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (dtype != ROLLOUT_DTYPE_BF16 || max_splits <= 1) return 1;
   if (M <= kRingMaxRows) return ring_splits(N, K, max_splits);
-  // tile kernel: enough K splits for ~1.5 workgroups per CU, K slices of at least 512
   const int nwg = tile_m_tiles(M) * tile_n_tiles(N);
-  int s = (384 + nwg - 1) / nwg;
-  s = std::min(s, std::max(1, K / 512));
-  s = std::max(1, std::min(s, max_splits));
+  int s;
+  if (M <= 256) {
+    // decode-sized batches: workgroup x of a split runs on XCD x % 8, which holds N tiles nt % 8 == j for
+    // every M tile.  Split K until the busiest XCD holds one workgroup per CU (32); with long K slices
+    // (> 64 k-steps) two per CU.  Fewer splits leave CUs idle, more add partial-sum traffic and a second
+    // round of workgroups on the busiest XCD.
+    const int per_xcd = tile_m_tiles(M) * ((tile_n_tiles(N) + 7) / 8);
+    const int smax = std::max(1, std::min(max_splits, K / 256));
+    s = std::max(1, std::min(smax, 32 / per_xcd));
+    if (K / 32 / s > 64) s = std::max(s, std::min(smax, 64 / per_xcd));
+  } else {
+    // MFMA-bound batches: enough K splits for ~1.5 workgroups per CU, K slices of at least 512
+    s = (384 + nwg - 1) / nwg;
+    s = std::min(s, std::max(1, K / 512));
+    s = std::max(1, std::min(s, max_splits));
+  }
   const int ks = kslice_for(K, s);
   return (K + ks - 1) / ks;
 }
