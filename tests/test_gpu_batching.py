@@ -99,12 +99,15 @@ def test_tiny_fp32_eos_without_stop_set_equals_generate(whole_groups, P):
     eng.close()
 
 
-@pytest.mark.parametrize("refill,slots,whole_groups,P", [(1, 8, 1, 40), (4, 16, 1, 40), (2, 4, 1, 40),
-                                                         (1, 8, 0, 40), (3, 12, 0, 32), (2, 5, 0, 40)])
-def test_bf16_eos_schedule_and_stop_rule(refill, slots, whole_groups, P):
+@pytest.mark.parametrize("refill,slots,whole_groups,P,shared", [
+    (1, 8, 1, 40, "1"), (4, 16, 1, 40, "1"), (2, 4, 1, 40, "1"), (2, 8, 1, 40, "2"), (3, 16, 1, 32, "2"),
+    (1, 8, 0, 40, "1"), (3, 12, 0, 32, "1"), (2, 5, 0, 40, "2")])
+def test_bf16_eos_schedule_and_stop_rule(refill, slots, whole_groups, P, shared, monkeypatch):
+    # shared = "2" forces the shared-prefix attention wherever whole groups make it possible
+    monkeypatch.setenv("ROLLOUT_SHARED_PREFIX", shared)
     G, n_prompts, N = 4, 7, 24
     log(f"bf16 small GQA eos: {n_prompts} prompts x G={G}, {slots} slots, refill every {refill}, "
-        f"whole_groups={whole_groups}, P={P}")
+        f"whole_groups={whole_groups}, P={P}, shared prefix {shared}")
     cfg = R.model_config(SMALL_BF16, R.DTYPE_BF16, P, N, 2 * slots + G)
     eng = R.Engine(cfg, group_size=G)
     prompts = W.prompts(n_prompts, P, cfg.vocab, seed=61)
