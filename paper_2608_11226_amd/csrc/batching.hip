@@ -4,7 +4,7 @@
 // The paper's controller counts T_k, the non-padding tokens a generation batch
 // yields (section 4.5, eq. 4), and its runs reward closeness to a 128-token
 // completion length (section 5); both need completions that end when a stop
-// token is drawn.  Slots hold whole groups (section 4.3).  Per slot r the
+// token is drawn.  Per slot r the
 // device keeps the completion it serves (seq[r], -1 for none), the next token
 // column (col[r]) and an ended flag (done[r]).  The decode step draws into a
 // slot-indexed buffer (draw[r], with the slot's staged uniform u_slot[r]);
@@ -51,10 +51,10 @@ __global__ void k_cb_reset(int S, int32_t* __restrict__ seq, int32_t* __restrict
 __global__ void k_cb_admit(int r0, int G, int seq0, int P, int N, int32_t* __restrict__ seq,
                            int32_t* __restrict__ col, int32_t* __restrict__ done, int32_t* __restrict__ ctx_len,
                            int32_t* __restrict__ tokens_out) {
-  for (int i = threadIdx.x; i < G * N; i += blockDim.x) tokens_out[(size_t)seq0 * N + i] = -1;
-  if (threadIdx.x < G) {
-    const int r = r0 + threadIdx.x;
-    seq[r] = seq0 + threadIdx.x;
+  for (size_t i = threadIdx.x; i < (size_t)G * N; i += blockDim.x) tokens_out[(size_t)seq0 * N + i] = -1;
+  for (int g = threadIdx.x; g < G; g += blockDim.x) {
+    const int r = r0 + g;
+    seq[r] = seq0 + g;
     col[r] = 0;
     done[r] = 0;
     ctx_len[r] = P;

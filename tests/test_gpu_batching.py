@@ -171,3 +171,19 @@ def test_bad_stop_id_is_reported():
     with pytest.raises(R.RolloutError, match="outside"):
         eng.synchronize()
     eng.close()
+
+
+def test_whole_group_refill_with_groups_wider_than_a_workgroup():
+    # G = 260 slots per range: the admission kernel covers them all
+    G, n_prompts, P, N = 260, 3, 16, 6
+    cfg = R.model_config("tiny", R.DTYPE_FP32, P, N, G)
+    eng = R.Engine(cfg, group_size=G)
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=91)
+    u = W.uniforms(n_prompts * G, N, seed=92)
+    stop = list(range(0, cfg.vocab, 4))
+    tok, L, admit, steps = _run_eos(eng, prompts, G, G, N, 1.0, 1.0, u, stop, 1, 1)
+    _check_structure(tok, L, stop, N, cfg.vocab)
+    want_admit, want_steps = _expected_schedule(L, G, G, 1, 1)
+    assert list(admit) == list(want_admit) and steps == want_steps
+    assert sorted(set(admit.tolist())) == sorted(set(want_admit.tolist())) and len(set(admit.tolist())) == 3
+    eng.close()
