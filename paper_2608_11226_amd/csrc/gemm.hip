@@ -201,6 +201,17 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
   const int per = (nkw + KW - 1) / KW;
   const int kb0 = kw0 + wave * per;
   const int nk = min(kw0 + nkw, kb0 + per) - kb0;         // this wave's k-steps; an empty share adds zeros
+  if constexpr (KW == 1) {
+    if (nk <= 0) {  // an empty K split contributes zeros
+      if constexpr (!SWI) {
+        for (int j = 0; j < NBW && nb0 + j < nbt; ++j)
+          for (int m = lane & 15; m < M; m += 16)
+            *reinterpret_cast<float4*>(out + ((size_t)blockIdx.y * M + m) * N + (nb0 + j) * 16 + 4 * (lane >> 4)) =
+                make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      return;
+    }
+  }
   floatx4_t acc[NBW][MB];
 #pragma unroll
   for (int j = 0; j < NBW; ++j)
