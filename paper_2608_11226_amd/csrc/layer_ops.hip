@@ -74,6 +74,53 @@ __global__ __launch_bounds__(1024) void k_residual_norm(const float* __restrict_
   }
 }
 
+// The same for rows of at most 1024 groups of 8 columns (every model here): one thread per group keeps
+// its eight values in registers from load to store, and its loads of x, the gain and up to MAXS split
+// partials all go out at once (threads past the row repeat the last group's addresses and store nothing),
+// so a row costs one memory round trip, the block reduction and the stores.
+template <typename T, int MAXS>
+__global__ __launch_bounds__(1024) void k_residual_norm_row(const float* __restrict__ part, int splits, int M, int d,
+                                                            float* __restrict__ x, const float* __restrict__ gain,
+                                                            float eps, T* __restrict__ out) {
+  __shared__ float red[32];
+  const int m = blockIdx.x;
+  const int Mb = (M + 15) >> 4;
+  const int ng = d >> 3;
+  const bool act = (int)threadIdx.x < ng;
+  const size_t c = (size_t)(act ? threadIdx.x : ng - 1) * 8;
+  float* xr = x + (size_t)m * d;
+  float v[8], gn[8];
+  ld8(xr, c, v);
+  ld8(gain, c, gn);
+  if (part) {
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int s0 = 0; s0 < splits; s0 += MAXS) {
+      float p[MAXS][8];
+#pragma unroll
+      for (int s = 0; s < MAXS; ++s) ld8(part, ((size_t)min(s0 + s, splits - 1) * M + m) * d + c, p[s]);
+#pragma unroll
+      for (int s = 0; s < MAXS; ++s)
+        if (s0 + s < splits)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] += p[s][e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] += acc[e];
+    if (act) st8(xr, c, v);
+  }
+  float ss = 0.f;
+  if (act)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
+  const float tot = block_sum(ss, red);
+  const float r = 1.0f / sqrtf(tot / (float)d + eps);
+  if (act) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * r * gn[e];
+    st8(out, xoff(out, m, (int)c, d, Mb), v);
+  }
+}
+
 __device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int* pos) {
   if (rm.P > 0) {
     const int p = m / rm.P;
@@ -220,8 +267,26 @@ hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* 
 hipError_t launch_residual_norm(hipStream_t s, int dtype, const float* part, int splits, int M, int d, float* x,
                                 const float* gain, float eps, void* out) {
   if (M <= 0) return hipSuccess;
+  const int ng = d >> 3;
   // one thread per group of 8 columns (up to 1024 threads per row)
-  const int threads = std::min(1024, ((d >> 3) + 63) / 64 * 64);
+  const int threads = std::min(1024, (ng + 63) / 64 * 64);
+  if (ng <= 1024) {
+    const bool bf = dtype == ROLLOUT_DTYPE_BF16;
+#define ROLLOUT_NORM_ROW(S)                                                                                           \
+  do {                                                                                                                \
+    if (bf)                                                                                                           \
+      hipLaunchKernelGGL((k_residual_norm_row<uint16_t, S>), dim3(M), dim3(threads), 0, s, part, splits, M, d, x,    \
+                         gain, eps, (uint16_t*)out);                                                                  \
+    else                                                                                                              \
+      hipLaunchKernelGGL((k_residual_norm_row<float, S>), dim3(M), dim3(threads), 0, s, part, splits, M, d, x, gain, \
+                         eps, (float*)out);                                                                           \
+  } while (0)
+    if (!part || splits <= 1) ROLLOUT_NORM_ROW(1);
+    else if (splits <= 4) ROLLOUT_NORM_ROW(4);
+    else ROLLOUT_NORM_ROW(8);
+#undef ROLLOUT_NORM_ROW
+    return hipGetLastError();
+  }
   if (dtype == ROLLOUT_DTYPE_BF16)
     hipLaunchKernelGGL(k_residual_norm<uint16_t>, dim3(M), dim3(threads), 0, s, part, splits, M, d, x, gain, eps,
                        (uint16_t*)out);
