@@ -635,15 +635,15 @@ bool mfma_attention(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 && (D.
 
 }  // namespace
 
-// Waves per decode-attention workgroup: eight when the grid is about one workgroup per CU (more loads in
-// flight per CU), four when there are at least two workgroups per CU to overlap each one's fixed phases
-// (q/k/v formation, merge) with the others' streaming.
-// ROLLOUT_ATTN_WAVES=4 or 8 forces the choice (read per call).
+// Waves per decode-attention workgroup: four once there is a workgroup per CU.  With that many
+// workgroups the KV stream runs near the HBM rate either way, and four waves halve the merge of the
+// waves' softmax states (7B, 256 workgroups: rollout +0.5% over eight).  Eight for smaller grids, which
+// need the loads of more waves in flight.  ROLLOUT_ATTN_WAVES=4 or 8 forces the choice (read per call).
 int attn_waves(int n_workgroups) {
   const char* v = std::getenv("ROLLOUT_ATTN_WAVES");
   const int forced = v ? std::atoi(v) : 0;
   if (forced == 4 || forced == 8) return forced;
-  return n_workgroups >= 512 ? 4 : 8;
+  return n_workgroups >= 256 ? 4 : 8;
 }
 
 bool attention_shares_prefix(const Dims& D) { return mfma_attention(D); }

@@ -3,8 +3,10 @@
 // bf16 path (CDNA4 MFMA, v_mfma_f32_16x16x32_bf16).  Both operands live in
 // HBM in MFMA operand order, so every global load is a fully coalesced
 // 16-byte-per-lane read:
-//   W (A operand): tiles of 16 weight rows x 32 k, [N/16][K/32][64 lanes][8],
-//                  lane = row%16 + 16*((k%32)/8) -- written once at synthesis;
+//   W (A operand): fragments of 16 weight rows x 32 k (64 lanes x 8, lane =
+//                  row%16 + 16*((k%32)/8)), the four fragments of 4
+//                  consecutive row blocks adjacent at each k-step (wfrag) --
+//                  written once at synthesis;
 //   X (B operand): tiles of 32 k x 16 activation rows, [K/32][M/16][64][8],
 //                  lane = m%16 + 16*((k%32)/8) -- written by the producing
 //                  kernel (norm, SwiGLU, attention).
@@ -102,8 +104,13 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
   if (nk > 0) {
     // every load is unconditional: block and k indices are clamped into range, surplus k-steps are not computed
     const bf16x8_t* wp[kTileNB];
+    int ws[kTileNB];  // k-step stride of each block's fragments
 #pragma unroll
-    for (int j = 0; j < kTileNB; ++j) wp[j] = W + ((size_t)min(nb0 + j, nbt - 1) * kbt + kb0) * 64 + lane;
+    for (int j = 0; j < kTileNB; ++j) {
+      const int nb = min(nb0 + j, nbt - 1);
+      wp[j] = W + wfrag(nb, kb0, nbt, kbt) * 64 + lane;
+      ws[j] = wgroup_blocks(nb, nbt) * 64;
+    }
     const bf16x8_t* xp[kTileXPW];
 #pragma unroll
     for (int i = 0; i < kTileXPW; ++i)
@@ -113,7 +120,7 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
     auto load_w = [&](int slot, int st) {
       const size_t kk = (size_t)min(st, nk - 1);
 #pragma unroll
-      for (int j = 0; j < kTileNB; ++j) wr[slot][j] = wp[j][kk * 64];
+      for (int j = 0; j < kTileNB; ++j) wr[slot][j] = wp[j][kk * ws[j]];
     };
     auto load_x = [&](int slot, int st) {
       const size_t kk = (size_t)min(st, nk - 1);
@@ -219,8 +226,13 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
     for (int mb = 0; mb < MB; ++mb) acc[j][mb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   if (nk > 0) {
     const bf16x8_t* wp[NBW];
+    int ws[NBW];  // k-step stride of each block's fragments
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) wp[j] = W + ((size_t)min(nb0 + j, nbt - 1) * kbt + kb0) * 64 + lane;
+    for (int j = 0; j < NBW; ++j) {
+      const int nb = min(nb0 + j, nbt - 1);
+      wp[j] = W + wfrag(nb, kb0, nbt, kbt) * 64 + lane;
+      ws[j] = wgroup_blocks(nb, nbt) * 64;
+    }
     const bf16x8_t* xp = XF + (size_t)kb0 * MB * 64 + lane;
     bf16x8_t wr[D][NBW], xr[D][MB];
     // ring stage d holds k-step min(i, nk - 1); steps past nk reload the last one and are not used
@@ -230,7 +242,7 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) xr[d][mb] = xp[(kk * MB + mb) * 64];
 #pragma unroll
-      for (int j = 0; j < NBW; ++j) wr[d][j] = __builtin_nontemporal_load(wp[j] + kk * 64);
+      for (int j = 0; j < NBW; ++j) wr[d][j] = __builtin_nontemporal_load(wp[j] + kk * ws[j]);
       __builtin_amdgcn_sched_barrier(0);
     }
     for (int i = 0; i < nk; i += D) {
@@ -247,7 +259,7 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) xr[d][mb] = xp[(kk * MB + mb) * 64];
 #pragma unroll
-        for (int j = 0; j < NBW; ++j) wr[d][j] = __builtin_nontemporal_load(wp[j] + kk * 64);
+        for (int j = 0; j < NBW; ++j) wr[d][j] = __builtin_nontemporal_load(wp[j] + kk * ws[j]);
         // keeps the ring order through scheduling, so each stage waits only for its own loads
         __builtin_amdgcn_sched_barrier(0);
       }

@@ -29,7 +29,7 @@ inline size_t elem_bytes(int dtype) { return dtype == ROLLOUT_DTYPE_BF16 ? 2 : 4
 // Physical layout of a weight matrix.
 enum WLayout : int {
   W_ROWMAJOR = 0,  // [rows][cols]
-  W_TILED = 1,     // MFMA operand tiles [rows/16][cols/32][64 lanes][8], lane = r%16 + 16*((c%32)/8)
+  W_TILED = 1,     // MFMA operand fragments, four 16-row blocks interleaved per k-step (wfrag)
 };
 
 // How physical rows of a (possibly fused) matrix map to synthesis tensor ids.
@@ -174,6 +174,29 @@ __device__ __forceinline__ float ldf(const float* p, size_t i) { return p[i]; }
 __device__ __forceinline__ float ldf(const uint16_t* p, size_t i) { return bf16_to_f32(p[i]); }
 __device__ __forceinline__ void stf(float* p, size_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void stf(uint16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+
+// bf16 weight matrices (the GEMMs' A operand) are stored as fragments of 16
+// rows x 32 k (64 lanes x 8 values, lane = row%16 + 16*((k%32)/8)).  The
+// fragments of four consecutive 16-row blocks at one k-step are adjacent,
+// [ceil(N/64)][K/32][4][64][8] (a last group of r < 4 blocks holds r per
+// k-step), so a wave that owns four blocks reads one contiguous 4 KB run per
+// k-step.  wfrag: fragment index of block nb at k-step kb (nbt = N/16 blocks,
+// kbt = K/32 k-steps); the fragment's 64 lanes follow it.
+__host__ __device__ __forceinline__ int wgroup_blocks(int nb, int nbt) {
+  const int r = nbt - (nb & ~3);
+  return r < 4 ? r : 4;
+}
+__host__ __device__ __forceinline__ size_t wfrag(int nb, int kb, int nbt, int kbt) {
+  return (size_t)(nb >> 2) * (size_t)kbt * 4 + (size_t)kb * (size_t)wgroup_blocks(nb, nbt) + (size_t)(nb & 3);
+}
+__host__ __device__ __forceinline__ void wfrag_inv(size_t t, int nbt, int kbt, int* nb, int* kb) {
+  const size_t per = (size_t)kbt * 4;
+  const int g = (int)(t / per);
+  const int rem = (int)(t - (size_t)g * per);
+  const int r = wgroup_blocks(4 * g, nbt);
+  *kb = rem / r;
+  *nb = 4 * g + rem % r;
+}
 
 // Element (m, k) of an M x K GEMM activation operand.  bf16 operands are kept
 // in MFMA B-operand order, tiles of 32 k x 16 rows: [K/32][Mb][64 lanes][8],

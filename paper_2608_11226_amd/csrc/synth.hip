@@ -40,10 +40,8 @@ __device__ __forceinline__ float weight_value(uint64_t key, uint64_t i, double s
 __device__ __forceinline__ void phys_rc(const WeightDesc& w, size_t p, int* row, int* col) {
   if (w.layout == W_TILED) {
     const int lane = (int)((p >> 3) & 63);
-    const size_t tile = p >> 9;
-    const int kbs = w.cols / 32;
-    const int kb = (int)(tile % (size_t)kbs);
-    const int nb = (int)(tile / (size_t)kbs);
+    int nb, kb;
+    wfrag_inv(p >> 9, w.rows / 16, w.cols / 32, &nb, &kb);
     *row = nb * 16 + (lane & 15);
     *col = kb * 32 + (lane >> 4) * 8;
   } else {
@@ -184,7 +182,7 @@ __global__ void k_export_q4(Q4Ptrs qp, WeightDesc w, int which, int rows, float*
   }
 }
 
-// int4 matrix -> two bf16 MFMA A-operand tile matrices [N/16][K/32][64][8], hi = bf16(w) and
+// int4 matrix -> two bf16 MFMA A-operand matrices in the weight fragment layout (wfrag), hi = bf16(w) and
 // lo = bf16(w - hi) (w - hi is exact in fp32), for the batches the tile GEMM takes.
 __global__ void k_dequant_q4(Q4Ptrs qp, int rows, int cols, uint4* __restrict__ hi, uint4* __restrict__ lo) {
   const int kbt = cols / 32, gbt = cols / 128;
@@ -215,8 +213,9 @@ __global__ void k_dequant_q4(Q4Ptrs qp, int rows, int cols, uint4* __restrict__ 
       oh[t] = h2;
       ol[t] = l2;
     }
-    hi[i] = make_uint4(oh[0], oh[1], oh[2], oh[3]);
-    lo[i] = make_uint4(ol[0], ol[1], ol[2], ol[3]);
+    const size_t o = wfrag((int)nb, kb, rows / 16, kbt) * 64 + (size_t)lane;
+    hi[o] = make_uint4(oh[0], oh[1], oh[2], oh[3]);
+    lo[o] = make_uint4(ol[0], ol[1], ol[2], ol[3]);
   }
 }
 
@@ -237,7 +236,7 @@ __global__ void k_export(const T* __restrict__ src, WeightDesc w, int which, int
     if (w.layout == W_TILED) {
       const int nb = prow >> 4, kb = c >> 5;
       const int lane = (prow & 15) + 16 * ((c & 31) >> 3);
-      p = (((size_t)nb * (size_t)(w.cols / 32) + (size_t)kb) * 64 + (size_t)lane) * 8 + (size_t)(c & 7);
+      p = (wfrag(nb, kb, w.rows / 16, w.cols / 32) * 64 + (size_t)lane) * 8 + (size_t)(c & 7);
     } else {
       p = (size_t)prow * (size_t)w.cols + (size_t)c;
     }
