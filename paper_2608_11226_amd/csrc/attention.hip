@@ -135,6 +135,7 @@ __device__ __forceinline__ void attend_tile(KVTile<HD>& t, const bf16x8_t* qf, i
 // then enters the softmax as one more state beside the waves' states, so no
 // wave reads the cache entry this workgroup is writing.
 constexpr int kMaxQkvSplits = 16;  // most QKV split partials the attention kernel sums
+constexpr int kQkvBatch = 8;       // of which the first this many are loaded with the block table
 constexpr int kMaxTableBlocks = 16384;
 
 struct AttnQKV {
@@ -187,38 +188,48 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
 
   int t_end = pos + 1;  // keys read from the cache
   if constexpr (FQ) t_end = pos;
-  // One round trip for everything that does not depend on the block table:
-  // the table itself, the row's rotary factors and the QKV split sums
-  // (one float4 column group per thread, every split's load in flight at once).
+  // One round trip for the block table, the row's rotary factors and the first kQkvBatch QKV split
+  // partials of this thread's column groups (float4 groups; every load in flight at once).  The table
+  // goes to LDS as soon as it arrives and the first K/V tiles go out before the partials are summed, so
+  // the waits on the partials (and the LDS-only barriers after them) leave the tile loads in flight.
   const int ntab = (t_end + blk - 1) / blk;
-  for (int i = tid; i < ntab; i += NT) s_tab[i] = trow[i];
+  constexpr int GI = (18 * (HD / 4) + NT - 1) / NT;  // column groups per thread (nrep <= 16)
+  const int ng = (nrep + 2) * (HD / 4);
+  const float* pr = FQ ? Q.part + (size_t)r * D.nqkv : nullptr;
+  const size_t split_stride = (size_t)R * D.nqkv;
+  const int s1 = FQ ? min(Q.splits, kQkvBatch) : 1;
+  float4 pv[FQ ? GI : 1][kQkvBatch];
+  auto group_col = [&](int gi) {
+    const int slot = gi / (HD / 4), i4 = (gi % (HD / 4)) * 4;
+    return (slot < nrep ? (kvh * nrep + slot) * HD : D.qd + (slot - nrep) * D.kvd + kvh * HD) + i4;
+  };
   if constexpr (FQ) {
+    // Every load here is unconditional (indices clamped; the clamped threads store the same value to
+    // the same LDS word as their neighbour), so the compiler's waits stay per load: the table store
+    // waits for the table alone and the partials stay in flight behind it.
     constexpr int half = HD / 2;
-    if (tid < HD) s_rope[tid] = tid < half ? Q.rope_cos[(size_t)pos * half + tid] : Q.rope_sin[(size_t)pos * half + tid - half];
-    const size_t n = D.nqkv, ss = (size_t)R * n;
-    const float* pr = Q.part + (size_t)r * n;
-    const int ng = (nrep + 2) * (HD / 4);
-    for (int gi = tid; gi < ng; gi += NT) {
-      const int slot = gi / (HD / 4), i4 = (gi % (HD / 4)) * 4;
-      const int c = (slot < nrep ? (kvh * nrep + slot) * HD : D.qd + (slot - nrep) * D.kvd + kvh * HD) + i4;
-      float4 v[kMaxQkvSplits];
+    for (int i = tid + NT; i < ntab; i += NT) s_tab[i] = trow[i];  // contexts of more than NT blocks
+    const int ti = min(tid, max(ntab - 1, 0));
+    const int tab0 = trow[ti];
+    __builtin_amdgcn_sched_barrier(0);
+    const int tr = min(tid, HD - 1);
+    const float rope0 = tr < half ? Q.rope_cos[(size_t)pos * half + tr] : Q.rope_sin[(size_t)pos * half + tr - half];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int sp = 0; sp < kMaxQkvSplits; ++sp)
-        v[sp] = *reinterpret_cast<const float4*>(pr + (size_t)min(sp, Q.splits - 1) * ss + c);
-      float4 acc = v[0];
+    for (int it = 0; it < GI; ++it) {
+      const int c = group_col(min(tid + it * NT, ng - 1));
 #pragma unroll
-      for (int sp = 1; sp < kMaxQkvSplits; ++sp) {
-        if (sp < Q.splits) {
-          acc.x += v[sp].x;
-          acc.y += v[sp].y;
-          acc.z += v[sp].z;
-          acc.w += v[sp].w;
-        }
-      }
-      *reinterpret_cast<float4*>(&s_raw[slot][i4]) = acc;
+      for (int sp = 0; sp < kQkvBatch; ++sp)
+        pv[it][sp] = *reinterpret_cast<const float4*>(pr + (size_t)min(sp, s1 - 1) * split_stride + c);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    s_tab[ti] = tab0;
+    s_rope[tr] = rope0;
+    lds_barrier();
+  } else {
+    for (int i = tid; i < ntab; i += NT) s_tab[i] = trow[i];
+    __syncthreads();
   }
-  __syncthreads();
 
   // wave w: tiles w, w + NW, ...  They pass through a ring of DR tiles in
   // registers: while one is attended, the next DR - 1 are loading.  The first
@@ -228,18 +239,53 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
   const int n_w = t_end > first ? (t_end - first + STRIDE - 1) / STRIDE : 0;
   bool bad = false;
   KVTile<HD> ring[DR];
-  if (n_w > 0) {
+  // unconditional, so that no branch sits between these loads and the waits for the partials: a wave
+  // with no tile here (n_w == 0) reloads tile 0's clamped rows and never uses them
+  if (FQ || n_w > 0) {
 #pragma unroll
     for (int d = 0; d < DR; ++d) {
-      load_tile<HD>(ring[d], first + STRIDE * min(d, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride, layer_base,
-                    blk_elems, n_blocks, &bad);
+      load_tile<HD>(ring[d], first + STRIDE * max(0, min(d, n_w - 1)), max(t_end, 1), hh, g, s_tab, blk, kv,
+                    block_stride, layer_base, blk_elems, n_blocks, &bad);
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (n_w == 0) bad = false;
   }
 
   // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
   bf16x8_t qf[KC];
   if constexpr (FQ) {
+    // split sums in split order: the first kQkvBatch from registers (threads past the last column
+    // group store group ng - 1 again), then any further partials, loaded now
+    float4 acc[GI];
+#pragma unroll
+    for (int it = 0; it < GI; ++it) {
+      acc[it] = pv[it][0];
+#pragma unroll
+      for (int sp = 1; sp < kQkvBatch; ++sp) {
+        if (sp < s1) {
+          acc[it].x += pv[it][sp].x;
+          acc[it].y += pv[it][sp].y;
+          acc[it].z += pv[it][sp].z;
+          acc[it].w += pv[it][sp].w;
+        }
+      }
+    }
+    for (int sp = kQkvBatch; sp < Q.splits; ++sp) {
+#pragma unroll
+      for (int it = 0; it < GI; ++it) {
+        const float4 t = *reinterpret_cast<const float4*>(pr + (size_t)sp * split_stride + group_col(min(tid + it * NT, ng - 1)));
+        acc[it].x += t.x;
+        acc[it].y += t.y;
+        acc[it].z += t.z;
+        acc[it].w += t.w;
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < GI; ++it) {
+      const int gi = min(tid + it * NT, ng - 1);
+      *reinterpret_cast<float4*>(&s_raw[gi / (HD / 4)][(gi % (HD / 4)) * 4]) = acc[it];
+    }
+    lds_barrier();
     // rotary embedding of q and k, bf16 rounding, cache append of k and v
     constexpr int half = HD / 2;
     const float* cs = s_rope;
@@ -279,7 +325,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
     }
     if (!bok && tid == 0) atomicOr(err, 2);
     for (int it = tid; it < (16 - nrep) * HD; it += NT) s_q[nrep + it / HD][it % HD] = 0;
-    __syncthreads();
+    lds_barrier();  // LDS only: the tile loads and the cache stores stay in flight
 #pragma unroll
     for (int c = 0; c < KC; ++c) qf[c] = *reinterpret_cast<const bf16x8_t*>(&s_q[hh][32 * c + 8 * g]);
     // score of the current token: one wave per head

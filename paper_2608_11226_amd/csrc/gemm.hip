@@ -67,11 +67,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-// LDS barrier: this wave's LDS writes are complete, then every wave of the workgroup has arrived.  Written
-// as one asm statement with a memory clobber so that no LDS access moves across it and no wait for
-// outstanding global loads (the register prefetch) is added.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
 // Tile kernel: 4 waves, 256 weight rows x 128 activation rows per workgroup, each wave 64 x 128.
 constexpr int kTileNB = 4;            // 16-row weight blocks per wave
 constexpr int kTileMB = 8;            // 16-row activation blocks per workgroup

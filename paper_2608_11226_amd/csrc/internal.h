@@ -238,6 +238,11 @@ __device__ __forceinline__ void ld8(const uint16_t* p, size_t i, float* v) {
   }
 }
 
+// LDS barrier: this wave's LDS writes are complete, then every wave of the workgroup has arrived.  Written
+// as one asm statement with a memory clobber so that no LDS access moves across it and no wait for
+// outstanding global memory operations (a register prefetch, stores) is added.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
