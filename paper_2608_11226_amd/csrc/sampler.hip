@@ -16,17 +16,21 @@
 // bit patterns of e (monotonic for e >= 0): four 8-bit digits, each digit
 // chosen from mass histograms.  Ties at tau are kept lowest id first.
 //
-// Every pass over a row's V values runs as rows x chunks workgroups (chunk
+// Two implementations of the same integers.  Chunked (fewer rows): every
+// pass over a row's V values runs as rows x chunks workgroups (chunk
 // max; exp stored once with the chunk mass and first-digit histogram; one
 // histogram pass per remaining digit; per-chunk kept mass and tie count);
 // between passes a small kernel per row picks the digit with a parallel
 // suffix scan over the 256 bins.  The final kernel per row scans the chunk
 // totals, finds the chunk holding the crossing, and walks only that chunk:
 // one contiguous segment per wave, segment totals scanned across waves, then
-// the crossing wave scans its segment 64 ids at a time.
+// the crossing wave scans its segment 64 ids at a time.  Per row (128 rows
+// and more): one workgroup makes all of these passes over its row.
 #include "internal.h"
 
 #include <climits>
+#include <cstdlib>
+#include <string>
 
 namespace rollout {
 namespace {
@@ -369,6 +373,274 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
   if (tid == 0) out[(size_t)row * out_stride + c_out] = s_tok < 0 ? 0 : s_tok;
 }
 
+// ---------------------------------------------------------------------------
+// One workgroup per row
+// ---------------------------------------------------------------------------
+// Rows of at most kRowMaxV ids (V a multiple of 4) are sampled by one
+// workgroup of SR threads that makes every pass above itself, so a step costs
+// one launch instead of up to eleven and no pass waits for another kernel.
+// The row is cut into segments of 256 ids; wave w takes segments w, w + SRW,
+// ..., each lane four consecutive ids (one 16-byte load).  Masses, histograms,
+// the digit selection, the tie rule and the draw are the same integers as in
+// the chunked kernels (segments play the role of chunks), so both paths give
+// the same token.
+constexpr int SR = 1024;
+constexpr int SRW = SR / 64;
+constexpr int kSeg = 256;
+constexpr int kRowMaxSeg = SR;  // one segment per thread in the scans
+constexpr int kRowMaxV = kRowMaxSeg * kSeg;
+
+// inclusive scan of one u64 per thread over the SR threads; *tot receives the total
+__device__ __forceinline__ u64 block_incl_scan(u64 v, u64* wtot, u64* tot) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_incl_scan(v, lane);
+  __syncthreads();
+  if (lane == 63) wtot[w] = v;
+  __syncthreads();
+  u64 before = 0, all = 0;
+  for (int j = 0; j < SRW; ++j) {
+    if (j < w) before += wtot[j];
+    all += wtot[j];
+  }
+  *tot = all;
+  return v + before;
+}
+
+// Segments are visited four at a time per wave (sg0 + j * SRW, j < 4): the four 16-byte loads are
+// unconditional (ids past the row read its last four values and are masked at use), so they are all in
+// flight before the first is used.
+constexpr int kSegBatch = 4;
+__device__ __forceinline__ void load_seg_batch(const float* row, int V, int sg0, int lane, float4* a, bool* ok) {
+#pragma unroll
+  for (int j = 0; j < kSegBatch; ++j) {
+    const int i = (sg0 + j * SRW) * kSeg + 4 * lane;
+    ok[j] = i < V;
+    a[j] = *reinterpret_cast<const float4*>(row + min(i, V - 4));
+  }
+}
+
+__global__ __launch_bounds__(SR) void k_sample_row(const float* __restrict__ logits, int V, float T, float top_p,
+                                                   int filter, float* __restrict__ escr, const float* __restrict__ u,
+                                                   int u_stride, const int32_t* __restrict__ col,
+                                                   int32_t* __restrict__ out, int out_stride) {
+  __shared__ u64 hist[SRW][256];
+  __shared__ u64 s_gt[kRowMaxSeg], s_ties[kRowMaxSeg];
+  __shared__ u64 wtot[SRW];
+  __shared__ float s_redf[SRW];
+  __shared__ int wcnt[4];
+  __shared__ u64 s_above, s_target, s_excl, s_ties_before;
+  __shared__ unsigned s_prefix, s_mask;
+  __shared__ int s_seg, s_tok;
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c_out = col ? col[0] : 0;
+  const float* z = logits + (size_t)row * V;
+  float* e_row = escr + (size_t)row * V;
+  const int nseg = (V + kSeg - 1) / kSeg;
+
+  // m = max of y = fp32(z / T)
+  float mx = -INFINITY;
+  for (int sg0 = w; sg0 < nseg; sg0 += kSegBatch * SRW) {
+    float4 a[kSegBatch];
+    bool ok[kSegBatch];
+    load_seg_batch(z, V, sg0, lane, a, ok);
+#pragma unroll
+    for (int j = 0; j < kSegBatch; ++j)
+      if (ok[j]) mx = fmaxf(mx, fmaxf(fmaxf(a[j].x / T, a[j].y / T), fmaxf(a[j].z / T, a[j].w / T)));
+  }
+  mx = wave_max(mx);
+  if (lane == 0) s_redf[w] = mx;
+  for (int i = tid; i < SRW * 256; i += SR) (&hist[0][0])[i] = 0;
+  if (tid == 0) {
+    s_seg = INT_MAX;
+    s_tok = -1;
+  }
+  __syncthreads();
+  float m = -INFINITY;
+  for (int j = 0; j < SRW; ++j) m = fmaxf(m, s_redf[j]);
+
+  // e = exp(y - m), stored; per-segment mass; first-digit (bits 24..31) mass histogram when filtering
+  for (int sg0 = w; sg0 < nseg; sg0 += kSegBatch * SRW) {
+    float4 a[kSegBatch];
+    bool ok[kSegBatch];
+    load_seg_batch(z, V, sg0, lane, a, ok);
+#pragma unroll
+    for (int j = 0; j < kSegBatch; ++j) {
+      const int sg = sg0 + j * SRW;
+      u64 f = 0;
+      if (ok[j]) {
+        const float e[4] = {expf(a[j].x / T - m), expf(a[j].y / T - m), expf(a[j].z / T - m), expf(a[j].w / T - m)};
+        *reinterpret_cast<float4*>(e_row + sg * kSeg + 4 * lane) = make_float4(e[0], e[1], e[2], e[3]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const u64 fq = fx40(e[q]);
+          f += fq;
+          if (filter) atomicAdd(&hist[w][__float_as_uint(e[q]) >> 24], fq);
+        }
+      }
+      f = wave_sum_u64(f);
+      if (lane == 0 && sg < nseg) {
+        s_gt[sg] = f;
+        s_ties[sg] = 0;
+      }
+    }
+  }
+  __syncthreads();
+  u64 total;
+  block_incl_scan(tid < nseg ? s_gt[tid] : 0, wtot, &total);
+
+  unsigned tau = 0;
+  u64 ftau = 0, kties = 0, kept = total;
+  if (filter) {
+    if (tid == 0) {
+      const u64 target = (u64)ceil((double)top_p * (double)total);
+      s_target = target > total ? total : (target == 0 ? 1 : target);
+      s_above = 0;
+      s_prefix = 0;
+      s_mask = 0;
+    }
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (shift != 24) {
+        // mass histogram of the digit at shift over the values matching the selected prefix
+        __syncthreads();
+        for (int i = tid; i < SRW * 256; i += SR) (&hist[0][0])[i] = 0;
+        __syncthreads();
+        const unsigned prefix = s_prefix, mask = s_mask;
+        for (int sg0 = w; sg0 < nseg; sg0 += kSegBatch * SRW) {
+          float4 a[kSegBatch];
+          bool ok[kSegBatch];
+          load_seg_batch(e_row, V, sg0, lane, a, ok);
+#pragma unroll
+          for (int j = 0; j < kSegBatch; ++j) {
+            if (!ok[j]) continue;
+            const float e[4] = {a[j].x, a[j].y, a[j].z, a[j].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const unsigned b = __float_as_uint(e[q]);
+              if ((b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(e[q]));
+            }
+          }
+        }
+      }
+      __syncthreads();
+      // the largest digit d with above + (mass of digits >= d) >= target; threads 0..255, thread t owning
+      // digit 255 - t, so the suffix sum is an inclusive scan in thread order
+      const int d = 255 - tid;
+      u64 h = 0, inc = 0;
+      if (tid < 256) {
+        for (int j = 0; j < SRW; ++j) h += hist[j][d];
+        inc = wave_incl_scan(h, lane);
+        if (lane == 63) wtot[w] = inc;
+      }
+      __syncthreads();
+      const u64 above = s_above, target = s_target;
+      if (tid < 256) {
+        for (int j = 0; j < w; ++j) inc += wtot[j];
+        const unsigned long long bal = __ballot(above + inc >= target);
+        if (lane == 0) wcnt[w] = __popcll(bal);
+      }
+      __syncthreads();
+      if (tid < 256 && d == wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3] - 1) {
+        s_above = above + inc - h;
+        s_prefix |= (unsigned)d << shift;
+        s_mask |= 255u << shift;
+      }
+    }
+    __syncthreads();
+    tau = s_prefix;
+    ftau = fx40(__uint_as_float(tau));
+    const u64 need = s_target - s_above;
+    kties = ftau ? (need + ftau - 1) / ftau : 0;
+    kept = s_above + kties * ftau;
+    // per segment: mass of the values above tau and the count of ties at tau
+    for (int sg0 = w; sg0 < nseg; sg0 += kSegBatch * SRW) {
+      float4 a[kSegBatch];
+      bool ok[kSegBatch];
+      load_seg_batch(e_row, V, sg0, lane, a, ok);
+#pragma unroll
+      for (int j = 0; j < kSegBatch; ++j) {
+        const int sg = sg0 + j * SRW;
+        u64 gt = 0, ties = 0;
+        if (ok[j]) {
+          const float e[4] = {a[j].x, a[j].y, a[j].z, a[j].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const unsigned b = __float_as_uint(e[q]);
+            if (b > tau) gt += fx40(e[q]);
+            else if (b == tau) ties += 1;
+          }
+        }
+        gt = wave_sum_u64(gt);
+        ties = wave_sum_u64(ties);
+        if (lane == 0 && sg < nseg) {
+          s_gt[sg] = gt;
+          s_ties[sg] = ties;
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // kept mass per segment (ties at tau kept lowest id first), its scan, and the segment holding the crossing
+  const u64 gt = tid < nseg ? s_gt[tid] : 0, ti = tid < nseg ? s_ties[tid] : 0;
+  u64 unused;
+  const u64 ties_before = block_incl_scan(ti, wtot, &unused) - ti;
+  const u64 kt = filter ? (kties > ties_before ? min(kties - ties_before, ti) : 0) : 0;
+  const u64 km = gt + kt * ftau;
+  const u64 incl = block_incl_scan(km, wtot, &unused);
+  // thresh < kept always (u < 1 and kept >= 2^40), so some segment holds the crossing
+  const u64 thresh = (u64)((double)u[(size_t)row * u_stride + c_out] * (double)kept);
+  if (tid < nseg && km > 0 && incl > thresh) atomicMin(&s_seg, tid);
+  __syncthreads();
+  const int c = s_seg == INT_MAX ? nseg - 1 : s_seg;
+  if (tid == c) {
+    s_excl = incl - km;
+    s_ties_before = ties_before;
+  }
+  __syncthreads();
+  if (w == 0) {
+    // walk the crossing segment 64 ids at a time
+    const int lo = c * kSeg, hi = min(V, lo + kSeg);
+    const u64 tb = s_ties_before, seg_ties = s_ties[c];
+    const u64 my_kept_ties = filter ? (kties > tb ? min(kties - tb, seg_ties) : 0) : 0;
+    u64 carry = s_excl, tie_carry = 0;
+    for (int base = lo; base < hi; base += 64) {
+      const int i = base + lane;
+      const float e = i < hi ? e_row[i] : 0.f;
+      const unsigned b = __float_as_uint(e);
+      bool keep = i < hi && (!filter || b > tau);
+      if (filter) {
+        const bool is_tie = i < hi && b == tau;
+        const u64 tie_incl = wave_incl_scan(is_tie ? 1ull : 0ull, lane);
+        if (is_tie && tie_carry + tie_incl - 1 < my_kept_ties) keep = true;
+        tie_carry += __shfl(tie_incl, 63, 64);
+      }
+      const u64 cum = carry + wave_incl_scan(keep ? fx40(e) : 0ull, lane);
+      const unsigned long long hit = __ballot(keep && cum > thresh);
+      if (hit) {
+        if (lane == __ffsll((long long)hit) - 1) s_tok = i;
+        break;
+      }
+      carry = __shfl(cum, 63, 64);
+    }
+  }
+  __syncthreads();
+  if (tid == 0) out[(size_t)row * out_stride + c_out] = s_tok < 0 ? 0 : s_tok;
+}
+
+// Which path samples S rows: one workgroup per row once there are kRowMinRows rows or more (its time is
+// set by one workgroup's passes over its row, so it barely grows with S; the chunked kernels grow with S
+// and win below).  Measured at V = 152064: S = 64, top-p 0.95: row 206 us, chunked 164 us; S = 256: row
+// 243 us, chunked 370 us (top-p 1: 79 / 67 and 91 / 203 us).  ROLLOUT_SAMPLE_PATH=row or =chunked
+// forces a path (read per call; the row path still needs V % 4 == 0 and V <= kRowMaxV).
+constexpr int kRowMinRows = 128;
+bool use_row_sampler(int S, int V) {
+  if (V % 4 != 0 || V > kRowMaxV) return false;
+  const char* v = std::getenv("ROLLOUT_SAMPLE_PATH");
+  if (v && std::string(v) == "row") return true;
+  if (v && std::string(v) == "chunked") return false;
+  return S >= kRowMinRows;
+}
+
 }  // namespace
 
 int sample_chunks(int V) {
@@ -408,6 +680,11 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
     return hipGetLastError();
   }
   const int filter = top_p < 1.0f;
+  if (use_row_sampler(S, V)) {
+    hipLaunchKernelGGL(k_sample_row, dim3(S), dim3(SR), 0, s, logits, V, temperature, top_p, filter, escr, u, u_stride,
+                       col, out, out_stride);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax);
   hipLaunchKernelGGL(k_chunk_exp, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass, chist,
                      filter);

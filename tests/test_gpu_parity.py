@@ -121,6 +121,39 @@ def test_sampler_matches_oracle(V, temperature, top_p):
     eng.close()
 
 
+@pytest.mark.parametrize("V", [1024, 2064, 152064])
+@pytest.mark.parametrize("temperature,top_p", [(1.0, 1.0), (0.9, 0.95), (0.7, 0.5), (1.0, 1e-6)])
+def test_sampler_row_kernel_equals_chunked_kernels(V, temperature, top_p, monkeypatch):
+    """The one-workgroup-per-row sampler and the chunked kernels draw the same token from the same logits
+    (same integer masses, digits, tie rule and draw), including value ties and a flat row."""
+    log(f"sampler paths V={V} T={temperature} top_p={top_p}")
+    S = 64
+    rng = np.random.default_rng(V + 7)
+    z = (rng.standard_normal((S, V)) * 2.0).astype(np.float32)
+    z[:8] = np.round(z[:8], 1)
+    z[8, :] = 0.5
+    z[9, : V // 2] = 3.0  # a tie at the maximum over half the row
+    u = W.uniforms(S, 1, seed=11)[:, 0]
+    u[10] = 0.0
+    u[11] = np.float32(1.0) - np.float32(2.0**-24)
+    cfg = R.model_config("tiny", R.DTYPE_FP32, 16, 8, 4)
+    cfg.vocab = V
+    eng = R.Engine(cfg)
+    dz = to_dev(z, torch)
+    du = to_dev(u, torch)
+    got = {}
+    for path in ("row", "chunked"):
+        monkeypatch.setenv("ROLLOUT_SAMPLE_PATH", path)
+        out = torch.full((S,), -1, dtype=torch.int32, device="cuda:0")
+        R.rollout_sample(eng.ctx, dz, S, temperature, top_p, du, out)
+        eng.synchronize()
+        got[path] = out.cpu().numpy()
+    monkeypatch.delenv("ROLLOUT_SAMPLE_PATH", raising=False)
+    assert (got["row"] >= 0).all() and (got["row"] < V).all()
+    assert np.array_equal(got["row"], got["chunked"]), np.nonzero(got["row"] != got["chunked"])
+    eng.close()
+
+
 # ---------------------------------------------------------------------------
 # tiny fp32 model: the whole rollout
 # ---------------------------------------------------------------------------
