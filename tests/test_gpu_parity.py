@@ -326,6 +326,39 @@ def test_bf16_gqa7_large_batch_teacher_forced_logits(monkeypatch):
         eng.close()
 
 
+# Shapes whose GEMMs have odd k-step counts and ragged weight groups: d_model 32 (one 32-wide k-step, so
+# the second wave of a two-wave decode workgroup has none), d_model 96 / d_ff 160 (3 and 5 k-steps, split
+# unevenly between the two waves), and row counts (QKV 160 = 10 blocks, vocab 208 = 13 blocks) that leave
+# the last four-block weight group short.  Prefill (72 rows) takes the tile GEMM, decode the ring.
+ODD_BF16 = [(1, 32, 1, 1, 32, 32, 64, 1e4), (2, 96, 3, 1, 32, 160, 208, 1e4)]
+
+
+@pytest.mark.parametrize("shape", ODD_BF16)
+def test_bf16_odd_k_steps_teacher_forced_logits(shape):
+    log(f"bf16 odd shape {shape} teacher forced")
+    n_prompts, G, P, N = 3, 4, 24, 5
+    S = n_prompts * G
+    cfg = R.model_config(shape, R.DTYPE_BF16, P, N, S)
+    eng = R.Engine(cfg)
+    model = OracleModel(shape_of(cfg), mode="bf16")
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=51)
+    u = W.uniforms(S, N, seed=52)
+    ref = rollout(model, prompts, G, N, 1.0, 1.0, u)
+    logits = torch.empty((S, cfg.vocab), dtype=torch.float32, device="cuda:0")
+    R.rollout_prefill(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, logits)
+    eng.synchronize()
+    err = [float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][0])))]
+    for t in range(1, N):
+        R.rollout_decode_step(eng.ctx, to_dev(ref["tokens"][:, t - 1], torch), logits)
+        eng.synchronize()
+        err.append(float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][t]))))
+    scale = float(np.max(np.abs(np.asarray(ref["logits"]))))
+    log(f"  max abs logit error per step: {['%.2e' % e for e in err]} (logits up to {scale:.3f})")
+    assert scale > 1e-2  # the comparison is not between near-zero logits
+    assert max(err) <= 3e-2
+    eng.close()
+
+
 def test_device_error_flag_on_bad_token():
     eng, cfg = _tiny_engine()
     prompts = W.prompts(2, 16, cfg.vocab)
