@@ -151,8 +151,12 @@ struct AttnQKV {
   float* st_ml;  // [row][head][2]: max, sum of p
 };
 
-template <int HD, int NW, int DR, bool FQ, bool SPLIT = false>
-__global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
+// ONE: every column group of the q/k/v formation fits one per thread ((nrep + 2) * HD / 4 <= NW * 64), so
+// the partials of a single group are held (fewer registers, more workgroups per CU); else up to 16 query
+// heads per KV head.
+template <int HD, int NW, int DR, bool FQ, bool SPLIT = false, bool ONE = false>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(ONE && NW == 4 ? 3 : 1)))
+void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
                                                        uint16_t* __restrict__ kv, int n_blocks,
                                                        const int32_t* __restrict__ tables, int max_blocks, RowMap rm,
                                                        int R, int layer, AttnQKV Q, uint16_t* __restrict__ out,
@@ -188,17 +192,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
 
   int t_end = pos + 1;  // keys read from the cache
   if constexpr (FQ) t_end = pos;
-  // One round trip for the block table, the row's rotary factors and the first kQkvBatch QKV split
+  // One round trip for the block table, the row's rotary factors and the first QB QKV split
   // partials of this thread's column groups (float4 groups; every load in flight at once).  The table
   // goes to LDS as soon as it arrives and the first K/V tiles go out before the partials are summed, so
   // the waits on the partials (and the LDS-only barriers after them) leave the tile loads in flight.
   const int ntab = (t_end + blk - 1) / blk;
-  constexpr int GI = (18 * (HD / 4) + NT - 1) / NT;  // column groups per thread (nrep <= 16)
+  constexpr int GI = ONE ? 1 : (18 * (HD / 4) + NT - 1) / NT;  // column groups per thread (nrep <= 16)
+  constexpr int QB = ONE ? kQkvBatch / 2 : kQkvBatch;              // partials loaded with the table
   const int ng = (nrep + 2) * (HD / 4);
   const float* pr = FQ ? Q.part + (size_t)r * D.nqkv : nullptr;
   const size_t split_stride = (size_t)R * D.nqkv;
-  const int s1 = FQ ? min(Q.splits, kQkvBatch) : 1;
-  float4 pv[FQ ? GI : 1][kQkvBatch];
+  const int s1 = FQ ? min(Q.splits, QB) : 1;
+  float4 pv[FQ ? GI : 1][QB];
   auto group_col = [&](int gi) {
     const int slot = gi / (HD / 4), i4 = (gi % (HD / 4)) * 4;
     return (slot < nrep ? (kvh * nrep + slot) * HD : D.qd + (slot - nrep) * D.kvd + kvh * HD) + i4;
@@ -219,7 +224,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
     for (int it = 0; it < GI; ++it) {
       const int c = group_col(min(tid + it * NT, ng - 1));
 #pragma unroll
-      for (int sp = 0; sp < kQkvBatch; ++sp)
+      for (int sp = 0; sp < QB; ++sp)
         pv[it][sp] = *reinterpret_cast<const float4*>(pr + (size_t)min(sp, s1 - 1) * split_stride + c);
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -254,14 +259,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
   // Q^T as the B operand: lane supplies head hh, dimensions 32c + 8g .. +7
   bf16x8_t qf[KC];
   if constexpr (FQ) {
-    // split sums in split order: the first kQkvBatch from registers (threads past the last column
+    // split sums in split order: the first QB from registers (threads past the last column
     // group store group ng - 1 again), then any further partials, loaded now
     float4 acc[GI];
 #pragma unroll
     for (int it = 0; it < GI; ++it) {
       acc[it] = pv[it][0];
 #pragma unroll
-      for (int sp = 1; sp < kQkvBatch; ++sp) {
+      for (int sp = 1; sp < QB; ++sp) {
         if (sp < s1) {
           acc[it].x += pv[it][sp].x;
           acc[it].y += pv[it][sp].y;
@@ -270,7 +275,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(Dims D, const uint16_t* _
         }
       }
     }
-    for (int sp = kQkvBatch; sp < Q.splits; ++sp) {
+    for (int sp = QB; sp < Q.splits; ++sp) {
 #pragma unroll
       for (int it = 0; it < GI; ++it) {
         const float4 t = *reinterpret_cast<const float4*>(pr + (size_t)sp * split_stride + group_col(min(tid + it * NT, ng - 1)));
@@ -677,6 +682,9 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ o
 }
 
 
+// whether the q/k/v column groups of one (row, KV head) fit one per thread of an NW-wave workgroup
+bool one_group(const Dims& D, int nw) { return (D.nh / D.nkv + 2) * (D.hd / 4) <= nw * 64; }
+
 bool mfma_attention(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 && (D.hd == 128 || D.hd == 64); }
 
 }  // namespace
@@ -709,8 +717,14 @@ hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, 
   const size_t tab_bytes = (size_t)max_blocks * 4;
   const dim3 sgrid((unsigned)R * D.nkv);
 #define ROLLOUT_SUFFIX(HD, NW)                                                                                       \
-  hipLaunchKernelGGL((k_attn_mfma<HD, NW, 2, true, true>), sgrid, dim3(NW * 64), tab_bytes, s, D,                     \
-                     (const uint16_t*)nullptr, kk, n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err)
+  do {                                                                                                               \
+    if (one_group(D, NW))                                                                                            \
+      hipLaunchKernelGGL((k_attn_mfma<HD, NW, 2, true, true, true>), sgrid, dim3(NW * 64), tab_bytes, s, D,          \
+                         (const uint16_t*)nullptr, kk, n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err);      \
+    else                                                                                                             \
+      hipLaunchKernelGGL((k_attn_mfma<HD, NW, 2, true, true>), sgrid, dim3(NW * 64), tab_bytes, s, D,                \
+                         (const uint16_t*)nullptr, kk, n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err);      \
+  } while (0)
   const int nws = attn_waves(R * D.nkv);
   if (D.hd == 128) {
     if (nws == 4) ROLLOUT_SUFFIX(128, 4);
@@ -774,8 +788,17 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
     uint16_t* oo = (uint16_t*)out;
     const size_t tab_bytes = (size_t)max_blocks * 4;
 #define ROLLOUT_MFMA_ATTN(HD, NW, DR, FQ)                                                                              \
-  hipLaunchKernelGGL((k_attn_mfma<HD, NW, DR, FQ>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk, n_blocks, tables, \
-                     max_blocks, rm, R, layer, Q, oo, err)
+  do {                                                                                                                 \
+    if constexpr (FQ && DR == 2) {                                                                                     \
+      if (one_group(D, NW)) {                                                                                          \
+        hipLaunchKernelGGL((k_attn_mfma<HD, NW, DR, FQ, false, true>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk,   \
+                           n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err);                                    \
+        break;                                                                                                         \
+      }                                                                                                                \
+    }                                                                                                                  \
+    hipLaunchKernelGGL((k_attn_mfma<HD, NW, DR, FQ>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk, n_blocks, tables,  \
+                       max_blocks, rm, R, layer, Q, oo, err);                                                          \
+  } while (0)
 #define ROLLOUT_MFMA_ATTN_NW(HD, FQ)                    \
   do {                                                  \
     if (nw == 4) ROLLOUT_MFMA_ATTN(HD, 4, 2, FQ);         \
