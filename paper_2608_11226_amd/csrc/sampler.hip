@@ -37,6 +37,7 @@ namespace {
 
 constexpr int CB = 256;  // threads of the per-chunk kernels
 constexpr int CW = CB / 64;
+constexpr int kMaxChunks = 64;  // chunks per row (sample_chunks caps nc here)
 constexpr int RB = 1024;  // threads of the per-row draw kernel
 constexpr int RW = RB / 64;
 typedef unsigned long long u64;
@@ -62,6 +63,18 @@ __device__ __forceinline__ u64 fx40(float e) {
   const int sh = ex - 110;  // e = mant * 2^(ex - 150)
   if (sh >= 0) return mant << sh;
   return sh > -24 ? mant >> (-sh) : 0;
+}
+
+// max of a row's nc chunk maxima, every load in flight at once (indices clamped, surplus masked)
+__device__ __forceinline__ float row_max(const float* cm, int nc) {
+  float v[kMaxChunks];
+#pragma unroll
+  for (int j = 0; j < kMaxChunks; ++j) v[j] = cm[min(j, nc - 1)];
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < kMaxChunks; ++j)
+    if (j < nc) m = fmaxf(m, v[j]);
+  return m;
 }
 
 __device__ __forceinline__ u64 wave_sum_u64(u64 v) {
@@ -147,8 +160,7 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
   __shared__ u64 hist[CW][256];
   __shared__ u64 red[CW];
   const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
-  float m = -INFINITY;
-  for (int j = 0; j < nc; ++j) m = fmaxf(m, cmax[(size_t)row * nc + j]);
+  const float m = row_max(cmax + (size_t)row * nc, nc);
   const float* z = logits + (size_t)row * V;
   float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
@@ -189,7 +201,14 @@ __global__ __launch_bounds__(256) void k_select_digit(const u64* __restrict__ ch
   RowSel st = sel[row];
   if (shift == 24) {  // first digit: initialise the row state from the chunk masses
     u64 total = 0;
-    for (int j = 0; j < nc; ++j) total += cmass[(size_t)row * nc + j];
+    {
+      u64 mv[kMaxChunks];
+#pragma unroll
+      for (int j = 0; j < kMaxChunks; ++j) mv[j] = cmass[(size_t)row * nc + min(j, nc - 1)];
+#pragma unroll
+      for (int j = 0; j < kMaxChunks; ++j)
+        if (j < nc) total += mv[j];
+    }
     st.total = total;
     u64 target = (u64)ceil((double)top_p * (double)total);
     st.target = target > total ? total : (target == 0 ? 1 : target);
@@ -199,7 +218,15 @@ __global__ __launch_bounds__(256) void k_select_digit(const u64* __restrict__ ch
   }
   const int d = 255 - tid;
   u64 h = 0;
-  for (int j = 0; j < nc; ++j) h += chist[((size_t)row * nc + j) * 256 + d];
+  {
+    // all nc chunk counts in flight at once (nc <= kMaxChunks; indices clamped, surplus masked)
+    u64 hv[kMaxChunks];
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) hv[j] = chist[((size_t)row * nc + min(j, nc - 1)) * 256 + d];
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j)
+      if (j < nc) h += hv[j];
+  }
   // inclusive scan in thread order = suffix sum over digits >= d
   u64 inc = wave_incl_scan(h, lane);
   if (lane == 63) wtot[w] = inc;
@@ -296,7 +323,12 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
     kties = st.kties;
     kept = st.kept;
   } else {
-    for (int j = 0; j < nc; ++j) kept += cmass[(size_t)row * nc + j];
+    u64 mv[kMaxChunks];
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) mv[j] = cmass[(size_t)row * nc + min(j, nc - 1)];
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j)
+      if (j < nc) kept += mv[j];
   }
   if (w == 0) {
     // chunk scan in one wave (nc <= 64): kept mass per chunk = gt + its kept ties
