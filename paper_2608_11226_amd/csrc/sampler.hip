@@ -661,8 +661,9 @@ __global__ __launch_bounds__(SR) void k_sample_row(const float* __restrict__ log
 
 // Which path samples S rows: one workgroup per row once there are kRowMinRows rows or more (its time is
 // set by one workgroup's passes over its row, so it barely grows with S; the chunked kernels grow with S
-// and win below).  Measured at V = 152064: S = 64, top-p 0.95: row 206 us, chunked 164 us; S = 256: row
-// 243 us, chunked 370 us (top-p 1: 79 / 67 and 91 / 203 us).  ROLLOUT_SAMPLE_PATH=row or =chunked
+// and win below).  Measured at V = 152064, row / chunked: S = 64, top-p 0.95: 208 / 147 us, top-p 1:
+// 79 / 75 us; S = 128: 211 / 205 and 80 / 108 us; S = 256: 248 / 375 and 92 / 226 us.
+// ROLLOUT_SAMPLE_PATH=row or =chunked
 // forces a path (read per call; the row path still needs V % 4 == 0 and V <= kRowMaxV).
 constexpr int kRowMinRows = 128;
 bool use_row_sampler(int S, int V) {
