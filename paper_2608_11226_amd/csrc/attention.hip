@@ -173,8 +173,13 @@ void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
   __shared__ float s_cur[16];             // current token's scaled score per head
   extern __shared__ int s_tab[];          // the sequence's block table (dynamic, max_blocks entries)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kvh = blockIdx.x % D.nkv;
-  const int r = blockIdx.x / D.nkv;
+  // XCD-aware order (workgroup b runs on XCD b % 8, and the grid is a multiple of 8): each XCD takes a
+  // contiguous range of (row, KV head) items, so the rows of one group (or one prompt) -- which read the
+  // same prompt KV blocks -- fetch them into one L2 instead of all eight
+  const int item = (int)(blockIdx.x & 7) * (int)(gridDim.x >> 3) + (int)(blockIdx.x >> 3);
+  if (item >= R * D.nkv) return;
+  const int kvh = item % D.nkv;
+  const int r = item / D.nkv;
   int seq, pos;
   row_place(rm, r, &seq, &pos);
   const int nrep = D.nh / D.nkv;
@@ -426,7 +431,7 @@ void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
 // column (keys p_shared .. pos, current token included) and writes the
 // normalised output in the O-projection operand layout.
 template <int HD, int NW, int DR>
-__global__ __launch_bounds__(NW * 64) void k_attn_prefix(Dims D, const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW == 4 ? 3 : 1))) void k_attn_prefix(Dims D, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ kv, int n_blocks,
                                                          const int32_t* __restrict__ tables, int max_blocks,
                                                          int layer, int seq0, int G, int n_groups, int p_shared,
@@ -700,6 +705,9 @@ int attn_waves(int n_workgroups) {
   return n_workgroups >= 256 ? 4 : 8;
 }
 
+// k_attn_mfma grid: one workgroup per (row, KV head), rounded up to a multiple of the 8 XCDs
+static unsigned attn_grid(int R, const Dims& D) { return (unsigned)(R * D.nkv + 7) / 8 * 8; }
+
 bool attention_shares_prefix(const Dims& D) { return mfma_attention(D); }
 
 hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, int n_blocks, const int32_t* tables,
@@ -715,7 +723,7 @@ hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, 
   uint16_t* oo = (uint16_t*)out;
   // suffix: keys p_shared .. pos of every row, q/k/v formed, state kept
   const size_t tab_bytes = (size_t)max_blocks * 4;
-  const dim3 sgrid((unsigned)R * D.nkv);
+  const dim3 sgrid(attn_grid(R, D));
 #define ROLLOUT_SUFFIX(HD, NW)                                                                                       \
   do {                                                                                                               \
     if (one_group(D, NW))                                                                                            \
@@ -781,7 +789,7 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
       const int d = v ? std::atoi(v) : 2;
       return d == 3 || d == 4 ? d : 2;
     }();
-    const dim3 grid((unsigned)R * D.nkv);
+    const dim3 grid(attn_grid(R, D));
     const AttnQKV Q{qkv_part, qkv_splits, rope_cos, rope_sin, 0, nullptr, nullptr, nullptr};
     const uint16_t* qq = (const uint16_t*)q;
     uint16_t* kk = (uint16_t*)kv_pool;
