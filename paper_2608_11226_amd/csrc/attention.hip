@@ -34,6 +34,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef short short8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void row_place(const RowMap& rm, int m, int* seq, int* pos) {
@@ -126,6 +127,106 @@ __device__ __forceinline__ void attend_tile(KVTile<HD>& t, const bf16x8_t* qf, i
     o[j] *= alpha;
     o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(t.v[j], ph, o[j], 0, 0, 0);
     o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(t.v[j], pl, o[j], 0, 0, 0);
+  }
+}
+
+// Two tiles per softmax update: one max and one sum reduction for 32 tokens, and P.V as one
+// v_mfma_f32_16x16x32_bf16 per 16 output dimensions (twice the tokens of the 16x16x16 form at the same
+// issue cost).  The 32 reduction indices of that MFMA are the lane's four tokens of tile a followed by its
+// four tokens of tile c, in both operands: V^T is the two tiles' four-token fragments side by side and P
+// is the two tiles' probabilities, exactly as the scores come out of the two QK^T products.
+template <int HD>
+__device__ __forceinline__ void mask_tail(KVTile<HD>& t, int tb, int t_end, int g) {
+  if (tb + 16 > t_end) {  // the clamped rows of the last tile may hold stale data: keep them out of the MFMA
+    const int vm = t_end - (tb + 4 * g);
+#pragma unroll
+    for (int j = 0; j < HD / 16; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e >= vm) t.v[j][e] = 0;
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void attend_pair(KVTile<HD>& ta, KVTile<HD>& tc, const bf16x8_t* qf, int tba, int tbc,
+                                            int t_end, int g, float scale, float& m_run, float& l_run, floatx4_t* o) {
+  floatx4_t sa = {0.f, 0.f, 0.f, 0.f}, sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < HD / 32; ++c) {
+    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ta.k[c], qf[c], sa, 0, 0, 0);
+    sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tc.k[c], qf[c], sc, 0, 0, 0);
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sa[i] = (tba + 4 * g + i < t_end) ? sa[i] * scale : -INFINITY;
+    sc[i] = (tbc + 4 * g + i < t_end) ? sc[i] * scale : -INFINITY;
+    mx = fmaxf(mx, fmaxf(sa[i], sc[i]));
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(m_run, mx);
+  const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
+  float p[8], ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    p[i] = (sa[i] == -INFINITY) ? 0.f : expf(sa[i] - m_new);
+    p[4 + i] = (sc[i] == -INFINITY) ? 0.f : expf(sc[i] - m_new);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ps += p[i];
+  ps += __shfl_xor(ps, 16, 64);
+  ps += __shfl_xor(ps, 32, 64);
+  l_run = l_run * alpha + ps;
+  m_run = m_new;
+  mask_tail<HD>(ta, tba, t_end, g);
+  mask_tail<HD>(tc, tbc, t_end, g);
+  // p as hi + lo, two bf16 terms (see attend_tile)
+  short8_t ph, pl;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    ph[i] = f2bs(p[i]);
+    pl[i] = f2bs(p[i] - __uint_as_float((uint32_t)(uint16_t)ph[i] << 16));
+  }
+  const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, ph), bl = __builtin_bit_cast(bf16x8_t, pl);
+#pragma unroll
+  for (int j = 0; j < HD / 16; ++j) {
+    const bf16x8_t v = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(ta.v[j], tc.v[j], 0, 1, 2, 3, 4, 5, 6, 7));
+    o[j] *= alpha;
+    o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v, bh, o[j], 0, 0, 0);
+    o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v, bl, o[j], 0, 0, 0);
+  }
+}
+
+// One pass of wave-strided tiles through a ring of DR tiles: tile k of this wave starts at first + STRIDE k.
+// With pairs (U = 2), ring slots (d, d + 1) hold consecutive tiles of the wave and are attended together;
+// the pair's two reloads then go out together, so no tile is in flight while a wave computes.  That pays
+// where several waves share a SIMD (the one-group decode instance and the prefix pass, three workgroups
+// per CU: 14B rollout +1.5%) and not at one wave per SIMD, which has nothing else to overlap (7B -0.6%;
+// a ring of two pairs needs registers those instances do not have).
+template <int HD, int DR, int U>
+__device__ __forceinline__ void attend_ring(KVTile<HD>* ring, int n_w, int first, int STRIDE, int t_end, int hh, int g,
+                                            const int* s_tab, int blk, const uint16_t* kv, size_t block_stride,
+                                            size_t layer_base, size_t blk_elems, int n_blocks, bool* bad,
+                                            const bf16x8_t* qf, float scale, float& m_run, float& l_run,
+                                            floatx4_t* o) {
+  constexpr int UU = DR % U == 0 ? U : 1;  // an odd ring attends single tiles
+  for (int i = 0; i < n_w; i += DR) {
+#pragma unroll
+    for (int d = 0; d < DR; d += UU) {
+      if (i + d < n_w) {
+        if constexpr (UU == 2)
+          attend_pair<HD>(ring[d], ring[d + 1], qf, first + STRIDE * (i + d), first + STRIDE * (i + d + 1), t_end, g,
+                          scale, m_run, l_run, o);
+        else
+          attend_tile<HD>(ring[d], qf, first + STRIDE * (i + d), t_end, g, scale, m_run, l_run, o);
+      }
+#pragma unroll
+      for (int u = 0; u < UU; ++u)
+        load_tile<HD>(ring[d + u], first + STRIDE * min(i + d + u + DR, n_w - 1), t_end, hh, g, s_tab, blk, kv,
+                      block_stride, layer_base, blk_elems, n_blocks, bad);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 }
 
@@ -356,17 +457,9 @@ void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
 #pragma unroll
   for (int j = 0; j < DT; ++j) o[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (n_w > 0) {
-    for (int i = 0; i < n_w; i += DR) {
-#pragma unroll
-      for (int d = 0; d < DR; ++d) {
-        if (i + d < n_w) attend_tile<HD>(ring[d], qf, first + STRIDE * (i + d), t_end, g, scale, m_run, l_run, o);
-        load_tile<HD>(ring[d], first + STRIDE * min(i + d + DR, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride,
-                      layer_base, blk_elems, n_blocks, &bad);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-  }
+  if (n_w > 0)
+    attend_ring<HD, DR, ONE ? 2 : 1>(ring, n_w, first, STRIDE, t_end, hh, g, s_tab, blk, kv, block_stride,
+                                     layer_base, blk_elems, n_blocks, &bad, qf, scale, m_run, l_run, o);
   if (bad) atomicOr(err, 4);
 
   // merge the waves: o[j][i] is head hh at dimension 16 j + 4 g + i
@@ -490,15 +583,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW == 4
                     blk_elems, n_blocks, &bad);
       __builtin_amdgcn_sched_barrier(0);
     }
-    for (int i = 0; i < n_w; i += DR) {
-#pragma unroll
-      for (int d = 0; d < DR; ++d) {
-        if (i + d < n_w) attend_tile<HD>(ring[d], qf, first + STRIDE * (i + d), t_end, g, scale, m_run, l_run, o);
-        load_tile<HD>(ring[d], first + STRIDE * min(i + d + DR, n_w - 1), t_end, hh, g, s_tab, blk, kv, block_stride,
-                      layer_base, blk_elems, n_blocks, &bad);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
+    attend_ring<HD, DR, 2>(ring, n_w, first, STRIDE, t_end, hh, g, s_tab, blk, kv, block_stride, layer_base,
+                           blk_elems, n_blocks, &bad, qf, scale, m_run, l_run, o);
   }
   if (bad) atomicOr(err, 4);
   if (g == 0) {
