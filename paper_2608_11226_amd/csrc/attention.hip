@@ -24,7 +24,7 @@
 // stages K/V tiles in LDS; a combine kernel merges its splits with
 // log-sum-exp weights in split order.
 //
-// Cache block layout: [block][layer][kv head][K: blk x hd | V: hd x blk].
+// Cache layout: [layer][block][kv head][K: blk x hd | V: hd x blk] (kv_offset).
 #include <cstdlib>
 
 #include "internal.h"
@@ -288,8 +288,8 @@ void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
   const int blk = D.blk;
   const size_t blk_elems = (size_t)blk * HD;
   const size_t kv_head_stride = 2 * blk_elems;
-  const size_t layer_base = ((size_t)layer * D.nkv + kvh) * kv_head_stride;
-  const size_t block_stride = (size_t)D.L * D.nkv * kv_head_stride;
+  const size_t layer_base = kv_offset(layer, 0, kvh, n_blocks, D.nkv, kv_head_stride);
+  const size_t block_stride = (size_t)D.nkv * kv_head_stride;
   const int32_t* trow = tables + (size_t)seq * max_blocks;
   const float scale = 1.0f / sqrtf((float)HD);
   bf16x8_t zero8;
@@ -547,8 +547,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW == 4
   const int blk = D.blk;
   const size_t blk_elems = (size_t)blk * HD;
   const size_t kv_head_stride = 2 * blk_elems;
-  const size_t layer_base = ((size_t)layer * D.nkv + kvh) * kv_head_stride;
-  const size_t block_stride = (size_t)D.L * D.nkv * kv_head_stride;
+  const size_t layer_base = kv_offset(layer, 0, kvh, n_blocks, D.nkv, kv_head_stride);
+  const size_t block_stride = (size_t)D.nkv * kv_head_stride;
   const int32_t* trow = tables + (size_t)(seq0 + grp * G) * max_blocks;
   for (int i = tid; i < p_shared / blk; i += NT) s_tab[i] = trow[i];
   // this lane's query column: (row grp*G + c / nrep, head kvh*nrep + c % nrep)
@@ -678,7 +678,7 @@ __global__ __launch_bounds__(256) void k_attn_valu(Dims D, const T* __restrict__
       const int b = tables[(size_t)seq * max_blocks + tok / D.blk];
       float kval = 0.f, vval = 0.f;
       if (b >= 0 && b < n_blocks) {
-        const size_t base = (((size_t)b * D.L + layer) * D.nkv + kvh) * 2 * blk_elems;
+        const size_t base = kv_offset(layer, b, kvh, n_blocks, D.nkv, 2 * blk_elems);
         kval = ldf(kv, base + (size_t)(tok % D.blk) * HD + dd);
         vval = ldf(kv, base + blk_elems + (size_t)dd * D.blk + (tok % D.blk));
       } else if (dd == 0) {

@@ -120,6 +120,10 @@ hipError_t launch_attention_shared(hipStream_t s, const Dims& D, void* kv_pool, 
                                    int max_blocks, RowMap rm, int R, int layer, int G, int p_shared, void* q_keep,
                                    float* st_o, float* st_ml, void* out, int32_t* err, const float* qkv_part,
                                    int qkv_splits, const float* rope_cos, const float* rope_sin);
+// copies block src to block dst in every layer of the pool (n_blocks blocks, bytes_per_layer per block and
+// layer: all KV heads, K and V), for a sequence that starts from a copy of a shared partial block
+hipError_t launch_copy_kv_block(hipStream_t s, void* kv_pool, int n_blocks, int L, size_t bytes_per_layer, int src,
+                                int dst);
 hipError_t launch_gather_rows(hipStream_t s, int dtype, const void* src, int ld, int P, int G, int n_prompts,
                               void* dst);
 hipError_t launch_advance(hipStream_t s, int32_t* ctx_len, int S, int32_t* cols);
@@ -202,6 +206,15 @@ __host__ __device__ __forceinline__ void wfrag_inv(size_t t, int nbt, int kbt, i
 // in MFMA B-operand order, tiles of 32 k x 16 rows: [K/32][Mb][64 lanes][8],
 // lane = m%16 + 16*((k%32)/8), Mb = ceil(M/16); fp32 operands are row-major.
 // Eight consecutive k starting at a multiple of 8 are contiguous in both.
+// KV pool layout: [layer][block][KV head][K: blk x hd | V: hd x blk] (elements).  One layer's blocks are
+// contiguous, so the blocks a decode step's attention reads for one layer span the pool's 1/L share and
+// not all of it (fewer address-translation pages per layer: 7B attention KV loop -8%).  head_elems is
+// 2 * blk * hd; the offset is that of (layer, block, KV head).
+__host__ __device__ __forceinline__ size_t kv_offset(int layer, int block, int kvh, int n_blocks, int nkv,
+                                                     size_t head_elems) {
+  return (((size_t)layer * n_blocks + block) * nkv + kvh) * head_elems;
+}
+
 __device__ __forceinline__ size_t xoff(const uint16_t*, int m, int k, int K, int Mb) {
   (void)K;
   return ((size_t)((k >> 5) * Mb + (m >> 4)) * 64 + (size_t)((m & 15) + ((k & 31) >> 3) * 16)) * 8 + (k & 7);

@@ -173,7 +173,7 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue(Dims D, const float* __rest
         for (int c = 0; c < copies; ++c) {
           const int b = tables[(size_t)(seq + c) * max_blocks + pos / D.blk];
           if (b < 0 || b >= n_blocks) { atomicOr(err, 2); continue; }
-          T* dst = kv + ((((size_t)b * D.L + layer) * D.nkv + kslot) * 2) * blk_elems + (size_t)(pos % D.blk) * hd;
+          T* dst = kv + kv_offset(layer, b, kslot, n_blocks, D.nkv, 2 * blk_elems) + (size_t)(pos % D.blk) * hd;
           stf(dst, i, o1);
           stf(dst, i + half, o2);
         }
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue(Dims D, const float* __rest
       for (int c = 0; c < copies; ++c) {
         const int b = tables[(size_t)(seq + c) * max_blocks + pos / D.blk];
         if (b < 0 || b >= n_blocks) { atomicOr(err, 2); continue; }
-        T* dst = kv + ((((size_t)b * D.L + layer) * D.nkv + vslot) * 2 + 1) * blk_elems + (size_t)i * D.blk +
+        T* dst = kv + kv_offset(layer, b, vslot, n_blocks, D.nkv, 2 * blk_elems) + blk_elems + (size_t)i * D.blk +
                  (pos % D.blk);
         stf(dst, 0, v);
       }
@@ -317,6 +317,24 @@ hipError_t launch_swiglu(hipStream_t s, int dtype, const float* part, int splits
     hipLaunchKernelGGL(k_swiglu<uint16_t>, grid, dim3(256), 0, s, part, splits, M, ff, (uint16_t*)h);
   else
     hipLaunchKernelGGL(k_swiglu<float>, grid, dim3(256), 0, s, part, splits, M, ff, (float*)h);
+  return hipGetLastError();
+}
+
+// one workgroup per layer copies block src's 16-byte words to block dst
+__global__ __launch_bounds__(256) void k_copy_kv_block(uint4* __restrict__ kv, size_t block_words, int n_blocks, int src,
+                                                       int dst) {
+  const size_t base = (size_t)blockIdx.x * n_blocks * block_words;
+  const uint4* from = kv + base + (size_t)src * block_words;
+  uint4* to = kv + base + (size_t)dst * block_words;
+  for (size_t i = threadIdx.x; i < block_words; i += blockDim.x) to[i] = from[i];
+}
+
+hipError_t launch_copy_kv_block(hipStream_t s, void* kv_pool, int n_blocks, int L, size_t bytes_per_layer, int src,
+                                int dst) {
+  if (L <= 0 || bytes_per_layer % 16 || src < 0 || src >= n_blocks || dst < 0 || dst >= n_blocks)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_copy_kv_block, dim3(L), dim3(256), 0, s, (uint4*)kv_pool, bytes_per_layer / 16, n_blocks, src,
+                     dst);
   return hipGetLastError();
 }
 

@@ -945,12 +945,10 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
     const int k = rec_of[p];
     HIP_TRY(ctx, launch_seq_table(ctx->stream, tables, Lo.max_blocks, r, k * n_rec, n_shared, partial, own0 + r * n_own,
                                   n_own), "slot table");
-    if (partial) {  // the slot's first own block starts as the record's copy of the partial prompt block
-      char* kvp = ctx->arena + Lo.work_end;
-      HIP_TRY(ctx, hipMemcpyAsync(kvp + (size_t)(own0 + r * n_own) * Lo.kv_block_bytes,
-                                  kvp + (size_t)(k * n_rec + n_shared) * Lo.kv_block_bytes, Lo.kv_block_bytes,
-                                  hipMemcpyDeviceToDevice, ctx->stream), "partial block");
-    }
+    if (partial)  // the slot's first own block starts as the record's copy of the partial prompt block
+      HIP_TRY(ctx, launch_copy_kv_block(ctx->stream, ctx->arena + Lo.work_end, ctx->n_blocks, D.L,
+                                        Lo.kv_block_bytes / D.L, k * n_rec + n_shared, own0 + r * n_own),
+              "partial block");
     HIP_TRY(ctx, launch_seq_admit(ctx->stream, cb, r, s, P, N, ctx_len, d_tokens_out), "admit");
     HIP_TRY(ctx, launch_cb_commit(ctx->stream, cb, r, r + 1, N, stop, d_uniforms, ctx_len, d_tokens_out, d_lengths_out,
                                   false), "commit");
