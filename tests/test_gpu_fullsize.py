@@ -2,11 +2,14 @@
 GPU in that benchmark's launch configuration, against the oracle on sampled outputs.
 
 * 7B-class (d 3584, GQA 28/4 x 128, FFN 18944, vocabulary 152064): 8 prompts x 256 tokens, G = 8, 64
-  sequences -- prefill at M = 2048 on the tile GEMM, decode at M = 64 on the ring GEMMs and the 8-wave
-  decode attention, the full LM head.
+  sequences -- prefill at M = 2048 on the tile GEMM, decode at M = 64 on the ring GEMMs and the 4-wave
+  decode attention (256 workgroups), the full LM head.
 * 14B-class (d 5120, GQA 40/8 x 128, FFN 13824): 16 prompts x 512 tokens, G = 16, 256 sequences -- prefill
   at M = 8192, decode at M = 256 on the tile GEMM (split K; gate/up with SwiGLU in the epilogue), the
-  shared-prefix attention (suffix and prefix passes, 4-wave workgroups).
+  shared-prefix attention (suffix and prefix passes, 4-wave workgroups, two tiles per softmax update).
+* 72B-class (d 8192, GQA 64/8 x 128, FFN 29568): 8 prompts x 512 tokens, G = 8, 64 sequences -- prefill
+  at M = 4096, decode at M = 64 on the ring GEMMs (gate/up N = 59136), the 4-wave decode attention with
+  eight query heads per KV head (512 workgroups, two per CU).
 
 The oracle is fed only what the compared outputs need: the embedding rows of the tokens used and the
 LM-head rows of a sample of vocabulary ids (both from the seeded generator, like the device's own
@@ -30,6 +33,7 @@ CASES = {
     # name: (shape, prompts, prompt length, G, prompts compared on the oracle)
     "7b": (W.ModelShape(1, 3584, 28, 4, 128, 18944, 152064, 1e-6, 1e6), 8, 256, 8, range(8)),
     "14b": (W.ModelShape(1, 5120, 40, 8, 128, 13824, 152064, 1e-6, 1e6), 16, 512, 16, (0, 5, 10, 15)),
+    "72b": (W.ModelShape(1, 8192, 64, 8, 128, 29568, 152064, 1e-6, 1e6), 8, 512, 8, (0, 4, 7)),
 }
 
 
@@ -45,6 +49,7 @@ def _oracle(shape, token_ids, vocab_ids):
         if name.endswith("norm"):
             continue
         lw[name] = W.weight_matrix(0, W.tensor_id_layer(0, slot), *W.logical_shape(shape, name))
+        log(f"  oracle weight {name} {lw[name].shape} generated")
     w["layers"] = {0: lw}
     log("  oracle weights generated")
     model = OracleModel(shape, w, mode="bf16")
