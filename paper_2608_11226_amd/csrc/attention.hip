@@ -782,7 +782,7 @@ bool mfma_attention(const Dims& D) { return D.dtype == ROLLOUT_DTYPE_BF16 && (D.
 
 // Waves per decode-attention workgroup: four once there is a workgroup per CU.  With that many
 // workgroups the KV stream runs near the HBM rate either way, and four waves halve the merge of the
-// waves' softmax states (7B, 256 workgroups: rollout +0.5% over eight).  Eight for smaller grids, which
+// waves' softmax states (7B, 256 workgroups: decode +1.6% over eight).  Eight for smaller grids, which
 // need the loads of more waves in flight.  ROLLOUT_ATTN_WAVES=4 or 8 forces the choice (read per call).
 int attn_waves(int n_workgroups) {
   const char* v = std::getenv("ROLLOUT_ATTN_WAVES");
