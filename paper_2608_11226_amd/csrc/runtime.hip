@@ -788,12 +788,13 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
     HIP_TRY(ctx, launch_set_cols(ctx->stream, cols, 0, 1), "set cols");
     const bool use_graph = !ctx->prof.on;
     // cols[0] = column of the token fed in, cols[1] = column drawn; both move on after the draw
+    // the sequences' positions and the token columns move on together, in one launch after the draw
     auto step = [&]() -> rollout_status {
-      rollout_status rr = enqueue_decode(ctx, tok, N, cols, logits, prompt_len + N);
+      rollout_status rr = enqueue_decode(ctx, tok, N, cols, logits, prompt_len + N, false);
       if (rr) return rr;
       HIP_TRY(ctx, launch_sample(ctx->stream, logits, Sw, D.V, temperature, top_p, uu, N, cols + 1, tok, N,
                                  ctx->at(ctx->Lo.samp)), "sample");
-      HIP_TRY(ctx, launch_advance(ctx->stream, nullptr, 0, cols), "advance");
+      HIP_TRY(ctx, launch_advance(ctx->stream, ctx->at<int32_t>(ctx->Lo.ctx_len), ctx->S, cols), "advance");
       return ROLLOUT_OK;
     };
     if (!use_graph) {
