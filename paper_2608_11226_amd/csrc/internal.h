@@ -93,6 +93,11 @@ hipError_t launch_gemm_swiglu_q4(hipStream_t s, const void* X, const void* W, in
 
 hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
                         const int32_t* col, int M, int d, int V, float* x, int32_t* err);
+// x[m] = E[token m] and out[m] = rmsnorm(x[m]) * gain in one kernel (d <= 8192, else hipErrorInvalidValue and
+// nothing enqueued); the same values as launch_embed followed by launch_residual_norm with part NULL.
+hipError_t launch_embed_norm(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
+                             const int32_t* col, int M, int d, int V, float* x, const float* gain, float eps, void* out,
+                             int32_t* err);
 // x[m] += sum_s part[s][m] (part may be NULL); out[m] = rmsnorm(x[m]) * gain in the cache dtype.
 hipError_t launch_residual_norm(hipStream_t s, int dtype, const float* part, int splits, int M, int d, float* x,
                                 const float* gain, float eps, void* out);

@@ -252,6 +252,59 @@ __global__ void k_set_cols(int32_t* cols, int c0, int c1) {
 
 }  // namespace
 
+// Decode-step embedding fused with the first layer's RMSNorm: x[m] = E[token of row m] (fp32) and out[m] =
+// rmsnorm(x[m]) * gain in the GEMM operand layout, with the arithmetic of k_residual_norm_row (same thread
+// mapping and block sum), so the result is the embedding kernel followed by that norm.  One thread per group
+// of 8 columns (d <= 8192); a token outside [0, V) sets err bit 1 and reads row 0.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_embed_norm_row(const T* __restrict__ E, const int32_t* __restrict__ tokens,
+                                                         int tok_stride, const int32_t* __restrict__ col, int M, int d,
+                                                         int V, float* __restrict__ x, const float* __restrict__ gain,
+                                                         float eps, T* __restrict__ out, int32_t* __restrict__ err) {
+  __shared__ float red[32];
+  const int m = blockIdx.x;
+  const int Mb = (M + 15) >> 4;
+  const int ng = d >> 3;
+  const bool act = (int)threadIdx.x < ng;
+  const size_t c = (size_t)(act ? threadIdx.x : ng - 1) * 8;
+  int tok = tokens[(size_t)m * tok_stride + (col ? col[0] : 0)];
+  if (tok < 0 || tok >= V) {
+    if (threadIdx.x == 0) atomicOr(err, 1);
+    tok = 0;
+  }
+  float v[8], gn[8];
+  ld8(E, (size_t)tok * d + c, v);
+  ld8(gain, c, gn);
+  if (act) st8(x + (size_t)m * d, c, v);
+  float ss = 0.f;
+  if (act)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
+  const float tot = block_sum(ss, red);
+  const float r = 1.0f / sqrtf(tot / (float)d + eps);
+  if (act) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * r * gn[e];
+    st8(out, xoff(out, m, (int)c, d, Mb), v);
+  }
+}
+
+hipError_t launch_embed_norm(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
+                             const int32_t* col, int M, int d, int V, float* x, const float* gain, float eps, void* out,
+                             int32_t* err) {
+  if (M <= 0) return hipSuccess;
+  const int ng = d >> 3;
+  if (d % 8 || ng > 1024) return hipErrorInvalidValue;
+  const int threads = (ng + 63) / 64 * 64;
+  if (dtype == ROLLOUT_DTYPE_BF16)
+    hipLaunchKernelGGL(k_embed_norm_row<uint16_t>, dim3(M), dim3(threads), 0, s, (const uint16_t*)E, tokens,
+                       tok_stride, col, M, d, V, x, gain, eps, (uint16_t*)out, err);
+  else
+    hipLaunchKernelGGL(k_embed_norm_row<float>, dim3(M), dim3(threads), 0, s, (const float*)E, tokens, tok_stride,
+                       col, M, d, V, x, gain, eps, (float*)out, err);
+  return hipGetLastError();
+}
+
 hipError_t launch_embed(hipStream_t s, int dtype, const void* E, const int32_t* tokens, int tok_stride,
                         const int32_t* col, int M, int d, int V, float* x, int32_t* err) {
   if (M <= 0) return hipSuccess;

@@ -372,7 +372,9 @@ bool use_shared_prefix(const rollout_ctx* c, int M, const RowMap& rm) {
 
 // One transformer pass over M rows (prefill chunk or decode batch). On return
 // c->Lo.a holds the final-normed hidden states (cache dtype).
-rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max, double kv_tokens_read) {
+// normed: the first layer's norm output is already in place (decode steps embed and normalise in one kernel)
+rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max, double kv_tokens_read,
+                              bool normed = false) {
   const Dims& D = c->D;
   const Layout& Lo = c->Lo;
   float* x = c->at<float>(Lo.x);
@@ -389,7 +391,7 @@ rollout_status forward_layers(rollout_ctx* c, int M, RowMap rm, int attn_ctx_max
   const double eb = (double)elem_bytes(D.dtype);
   int st_tok;
   const int asplits = attn_splits(attn_ctx_max, &st_tok);
-  {
+  if (!normed) {
     Scope sc(c, 2, (double)M * D.d * (4 + eb), 0);
     HIP_TRY(c, launch_residual_norm(c->stream, D.dtype, nullptr, 1, M, D.d, x, c->at<float>(Lo.layers[0].attn_norm),
                                     D.eps, a), "rmsnorm");
@@ -524,13 +526,19 @@ rollout_status enqueue_decode(rollout_ctx* c, const int32_t* tokens, int tok_str
   const Dims& D = c->D;
   const Layout& Lo = c->Lo;
   const int S = c->S;
+  const bool fused = D.d % 8 == 0 && D.d / 8 <= 1024;  // embedding and the first norm in one kernel
   {
     Scope sc(c, 2, (double)S * D.d * (4 + elem_bytes(D.dtype)), 0);
-    HIP_TRY(c, launch_embed(c->stream, D.dtype, c->at(Lo.embed), tokens, tok_stride, col, S, D.d, D.V,
-                            c->at<float>(Lo.x), c->at<int32_t>(Lo.err)), "embed");
+    if (fused)
+      HIP_TRY(c, launch_embed_norm(c->stream, D.dtype, c->at(Lo.embed), tokens, tok_stride, col, S, D.d, D.V,
+                                   c->at<float>(Lo.x), c->at<float>(Lo.layers[0].attn_norm), D.eps, c->at(Lo.a),
+                                   c->at<int32_t>(Lo.err)), "embed + norm");
+    else
+      HIP_TRY(c, launch_embed(c->stream, D.dtype, c->at(Lo.embed), tokens, tok_stride, col, S, D.d, D.V,
+                              c->at<float>(Lo.x), c->at<int32_t>(Lo.err)), "embed");
   }
   RowMap rm{c->at<int32_t>(Lo.ctx_len), 0, 1, 0};
-  rollout_status r = forward_layers(c, S, rm, ctx_max, (double)S * (c->cur_len + 1));
+  rollout_status r = forward_layers(c, S, rm, ctx_max, (double)S * (c->cur_len + 1), fused);
   if (r) return r;
   int s;
   r = gemm(c, c->at(Lo.a), c->at(Lo.lm_head), d_logits, S, D.V, D.d, 1, &s);
