@@ -46,10 +46,13 @@ typedef int32_t rollout_status;
 #define ROLLOUT_DTYPE_BF16 1     /* bf16 weights/cache/GEMM operands, fp32 residual and logits */
 #define ROLLOUT_DTYPE_INT4 2     /* as BF16, but the layer projections (q, k, v, o, gate, up, down) are
                                     weight-only int4: groups of 128 inputs of one output row, each with an
-                                    fp32 scale s and zero point z, w = bf16((q - z) * s) (the AWQ storage
-                                    format of the 72B generation proxy, sections 5 and 6.6); embedding and
-                                    LM head stay bf16.  Needs d_model, n_heads*head_dim and d_ff to be
-                                    multiples of 128. */
+                                    fp32 scale s = (hi - lo) / 15 and a zero point z = rint(-lo / s) in
+                                    [0, 15], codes q = clamp(rint(w / s) + z, 0, 15) (the AWQ storage format
+                                    of the 72B generation proxy, sections 5 and 6.6, which fix no format).
+                                    The model multiplies with the group-quantised weight's plain value
+                                    (q - z) * s, never rounded to bf16: each group's scale multiplies its
+                                    integer dot product in fp32.  Embedding and LM head stay bf16.  Needs
+                                    d_model, n_heads*head_dim and d_ff to be multiples of 128. */
 
 typedef struct rollout_ctx rollout_ctx;
 
@@ -101,6 +104,8 @@ typedef struct {
 rollout_status rollout_plan(const rollout_model_config* cfg, int32_t group_size, rollout_plan_t* out);
 
 /*
+ * Set up the rollout engine of section 3's rollout phase: the model of section 5 (a dense decoder of the
+ * Qwen2.5 family, here with synthetic weights) resident in HBM, ready to generate groups of completions.
  * Bind a context to a caller-owned device arena of arena_bytes (>= the plan's
  * arena_bytes for group size 1 at cfg->max_seqs_in_flight, or the value
  * returned by rollout_plan for the group size that will be used), enqueue
@@ -113,6 +118,8 @@ rollout_status rollout_init(const rollout_model_config* cfg, void* d_arena, uint
                             void* hip_stream, rollout_ctx** out);
 
 /*
+ * Section 3's rollout phase, first forward: a batch of B prompts, each the prompt of a group of G
+ * candidate completions.
  * Start a wave: n_prompts prompts of prompt_len tokens (d_prompts, int32,
  * row-major [n_prompts, prompt_len]), each expanded to group_size sequences.
  * Each prompt is run through the model once; its KV blocks are shared by the
@@ -127,6 +134,8 @@ rollout_status rollout_prefill(rollout_ctx* ctx, const int32_t* d_prompts, int32
                                int32_t prompt_len, int32_t group_size, float* d_logits);
 
 /*
+ * One autoregressive step of section 3's rollout phase (every candidate of every group extends by one
+ * token; completion length is the knob of Table 4's third row, section 6.4).
  * One decode step of the current wave: append token d_tokens[s] (int32
  * [n_seqs]) to every sequence s at its next position and write the logits of
  * that position, fp32 [n_seqs, vocab], to d_logits.  n_seqs is the wave's
@@ -136,6 +145,8 @@ rollout_status rollout_prefill(rollout_ctx* ctx, const int32_t* d_prompts, int32
 rollout_status rollout_decode_step(rollout_ctx* ctx, const int32_t* d_tokens, float* d_logits);
 
 /*
+ * The draw that makes a group's G candidates differ (section 3: G sampled answers to the same prompt).
+ * The paper names no sampler settings; temperature and top-p are per-call knobs with the definition below.
  * Draw one token per row of d_logits (fp32 [n_seqs, vocab]) with one uniform
  * per row (d_uniforms, fp32 [n_seqs], values in [0, 1)) into d_tokens_out
  * (int32 [n_seqs]).  temperature 0 is greedy (lowest id among equal maxima).
@@ -204,7 +215,8 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
  *    slots; a slot whose completion has ended takes the next completion.  A
  *    group's prompt is prefilled once, when its first completion is admitted,
  *    into a prompt record of KV blocks shared by its members (at most slots + 1
- *    records are alive); every member's token 0 is drawn then.  Needs
+ *    records are alive); every member's token 0 is drawn then, so group_size
+ *    must not exceed the context's sequence rows (else ENOMEM).  Needs
  *    (slots + 1) * ceil(prompt / block) + slots * (blocks from the last full
  *    prompt block to the end) KV blocks; fewer slots are used if the pool is
  *    smaller.

@@ -15,7 +15,8 @@ import ctypes
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "librollout.so")
+# ROLLOUT_LIBRARY may name another build of the same library (the host-sanitizer build of build.py --sanitize)
+LIB_PATH = os.environ.get("ROLLOUT_LIBRARY") or os.path.join(_PKG, "librollout.so")
 
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 DTYPE_FP32, DTYPE_BF16, DTYPE_INT4 = 0, 1, 2

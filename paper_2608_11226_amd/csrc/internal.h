@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <string>
+
 #include "rollout.h"
 
 namespace rollout {
@@ -156,6 +158,10 @@ hipError_t launch_seq_admit(hipStream_t s, const CbState& cb, int r, int seq_id,
 hipError_t launch_set_cols(hipStream_t s, int32_t* cols, int c0, int c1);
 // Sampler scratch: stored e values of S rows plus per-chunk statistics.
 size_t sample_scratch_bytes(int S, int V);
+// largest row count whose sampler scratch fits in `bytes` (0 if not even one row does)
+int sample_rows_fitting(size_t bytes, int V);
+// sets the message rollout_last_error(NULL) returns on the calling thread
+void set_last_error(const std::string& msg);
 hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float temperature, float top_p,
                          const float* u, int u_stride, const int32_t* col, int32_t* out, int out_stride,
                          void* scratch);

@@ -8,7 +8,7 @@
 // (xoff) and, like the cached K/V, in the cache dtype (bf16 rounded to
 // nearest-even on the bf16 path).
 //
-// Cache block layout (blk tokens): [block][layer][kv head][K: blk x hd | V: hd x blk];
+// KV pool layout (blk tokens per block): [layer][block][kv head][K: blk x hd | V: hd x blk];
 // K is token-major, V is dimension-major so the attention kernel's P.V MFMA
 // reads four consecutive tokens of one dimension as one 8-byte load.
 #include <algorithm>

@@ -16,6 +16,8 @@
 #include <string>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "internal.h"
 
 using namespace rollout;
@@ -210,6 +212,15 @@ int64_t blocks_needed(int n_prompts, int G, int P, int ctx, int blk) {
   return (int64_t)n_prompts * shared + (int64_t)n_prompts * G * per_seq;
 }
 
+// roctx range over one entry point's host-side work (enqueueing, and the waits the call makes itself), so
+// that a profiler's marker trace shows prefill, decode, sampling and advantages as named spans
+struct Range {
+  explicit Range(const char* name) { roctxRangePush(name); }
+  ~Range() { roctxRangePop(); }
+  Range(const Range&) = delete;
+  Range& operator=(const Range&) = delete;
+};
+
 struct Prof {
   bool on = false;
   std::vector<hipEvent_t> ev;
@@ -230,8 +241,14 @@ struct rollout_ctx {
   int n_blocks = 0;
   std::string err;
 
-  // host staging (pinned) for block tables and context lengths
-  int32_t* h_tables = nullptr;
+  // host staging (pinned) for block tables and context lengths: two buffers used in turn, each with an
+  // event after the copy that reads it, so a wave's upload waits only for the copy of the upload before last
+  int32_t* h_tables[2] = {nullptr, nullptr};
+  hipEvent_t h_tables_ev[2] = {nullptr, nullptr};
+  int h_tables_next = 0;
+  // graph executables of finished waves whose replays may still be running, each with an event recorded
+  // after its last replay; destroyed once that event has completed
+  std::vector<std::pair<hipGraphExec_t, hipEvent_t>> retired;
   int32_t* h_done = nullptr;  // ended flags of the slots, read back at refill boundaries
 
   // current wave
@@ -247,6 +264,13 @@ struct rollout_ctx {
 
 namespace {
 
+}  // namespace
+
+// The calling thread's context-free error message (what rollout_last_error(NULL) returns).
+void rollout::set_last_error(const std::string& msg) { g_last_error = msg; }
+
+namespace {
+
 rollout_status fail(rollout_ctx* c, rollout_status st, const std::string& msg) {
   if (c) c->err = msg;
   g_last_error = msg;
@@ -255,6 +279,23 @@ rollout_status fail(rollout_ctx* c, rollout_status st, const std::string& msg) {
 
 rollout_status hip_fail(rollout_ctx* c, hipError_t e, const char* where) {
   return fail(c, ROLLOUT_EDEVICE, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+// Destroy the graph executables of earlier waves whose last replay has finished (all of them, after waiting,
+// when wait is set).
+void reap_graphs(rollout_ctx* c, bool wait) {
+  auto& r = c->retired;
+  size_t keep = 0;
+  for (size_t i = 0; i < r.size(); ++i) {
+    const bool done = wait ? hipEventSynchronize(r[i].second) == hipSuccess : hipEventQuery(r[i].second) == hipSuccess;
+    if (done || wait) {
+      hipGraphExecDestroy(r[i].first);
+      hipEventDestroy(r[i].second);
+    } else {
+      r[keep++] = r[i];
+    }
+  }
+  r.resize(keep);
 }
 
 #define HIP_TRY(ctx, expr, where)                  \
@@ -457,9 +498,11 @@ rollout_status upload_wave(rollout_ctx* c, int n_prompts, int P, int G) {
   if (need > c->n_blocks)
     return fail(c, ROLLOUT_ENOMEM, "wave needs " + std::to_string(need) + " KV blocks, pool has " +
                                        std::to_string(c->n_blocks));
-  // the staging buffer may still feed a copy of the previous wave
-  HIP_TRY(c, hipStreamSynchronize(c->stream), "stream sync");
-  int32_t* t = c->h_tables;
+  // the staging buffer used two uploads ago may still feed its copy: wait for that copy only
+  const int buf = c->h_tables_next;
+  c->h_tables_next ^= 1;
+  HIP_TRY(c, hipEventSynchronize(c->h_tables_ev[buf]), "staging wait");
+  int32_t* t = c->h_tables[buf];
   std::fill(t, t + (size_t)Lo.S * Lo.max_blocks, -1);
   const int shared = P / D.blk;
   const int nb_seq = (ctx + D.blk - 1) / D.blk;
@@ -476,6 +519,7 @@ rollout_status upload_wave(rollout_ctx* c, int n_prompts, int P, int G) {
   for (int s = 0; s < Lo.S; ++s) ctxl[s] = s < S ? P : 0;
   HIP_TRY(c, hipMemcpyAsync(c->at(Lo.tables), t, (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipMemcpyHostToDevice,
                             c->stream), "block table upload");
+  HIP_TRY(c, hipEventRecord(c->h_tables_ev[buf], c->stream), "staging event");
   c->wave = true;
   c->seq_refill = false;
   c->S = S;
@@ -646,7 +690,12 @@ rollout_status rollout_init(const rollout_model_config* cfg, void* d_arena, uint
     if (e != hipSuccess) { delete c; return fail(nullptr, ROLLOUT_EDEVICE, std::string("stream: ") + hipGetErrorString(e)); }
     c->own_stream = true;
   }
-  hipError_t e = hipHostMalloc((void**)&c->h_tables, (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipHostMallocDefault);
+  hipError_t e = hipSuccess;
+  for (int b = 0; b < 2 && e == hipSuccess; ++b) {
+    e = hipHostMalloc((void**)&c->h_tables[b], (size_t)Lo.S * (Lo.max_blocks + 1) * 4, hipHostMallocDefault);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->h_tables_ev[b], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(c->h_tables_ev[b], c->stream);
+  }
   if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_done, (size_t)Lo.S * 4, hipHostMallocDefault);
   if (e != hipSuccess) {
     rollout_destroy(c);
@@ -696,8 +745,12 @@ rollout_status rollout_init(const rollout_model_config* cfg, void* d_arena, uint
 void rollout_destroy(rollout_ctx* ctx) {
   if (!ctx) return;
   if (ctx->stream) hipStreamSynchronize(ctx->stream);
+  reap_graphs(ctx, true);
   for (hipEvent_t e : ctx->prof.ev) hipEventDestroy(e);
-  if (ctx->h_tables) hipHostFree(ctx->h_tables);
+  for (int b = 0; b < 2; ++b) {
+    if (ctx->h_tables[b]) hipHostFree(ctx->h_tables[b]);
+    if (ctx->h_tables_ev[b]) hipEventDestroy(ctx->h_tables_ev[b]);
+  }
   if (ctx->h_done) hipHostFree(ctx->h_done);
   if (ctx->own_stream) hipStreamDestroy(ctx->stream);
   delete ctx;
@@ -705,6 +758,7 @@ void rollout_destroy(rollout_ctx* ctx) {
 
 rollout_status rollout_prefill(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts, int32_t prompt_len,
                                int32_t group_size, float* d_logits) {
+  Range range("rollout_prefill");
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   if (!d_prompts || !d_logits) return fail(ctx, ROLLOUT_EINVAL, "prompts and logits must be non-NULL");
   if (n_prompts < 1 || group_size < 1) return fail(ctx, ROLLOUT_EINVAL, "n_prompts and group_size must be >= 1");
@@ -717,6 +771,7 @@ rollout_status rollout_prefill(rollout_ctx* ctx, const int32_t* d_prompts, int32
 }
 
 rollout_status rollout_decode_step(rollout_ctx* ctx, const int32_t* d_tokens, float* d_logits) {
+  Range range("rollout_decode_step");
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   if (!d_tokens || !d_logits) return fail(ctx, ROLLOUT_EINVAL, "tokens and logits must be non-NULL");
   if (!ctx->wave) return fail(ctx, ROLLOUT_ESTATE, "decode before prefill");
@@ -730,6 +785,7 @@ rollout_status rollout_decode_step(rollout_ctx* ctx, const int32_t* d_tokens, fl
 
 rollout_status rollout_sample(rollout_ctx* ctx, const float* d_logits, int32_t n_seqs, float temperature, float top_p,
                               const float* d_uniforms, int32_t* d_tokens_out) {
+  Range range("rollout_sample");
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   if (!d_logits || !d_uniforms || !d_tokens_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
   if (n_seqs < 1) return fail(ctx, ROLLOUT_EINVAL, "n_seqs must be >= 1");
@@ -747,6 +803,7 @@ rollout_status rollout_sample(rollout_ctx* ctx, const float* d_logits, int32_t n
 
 rollout_status grpo_advantages(const float* d_rewards, int32_t n_groups, int32_t group_size, float eps,
                                int32_t std_ddof, float* d_adv, int32_t* d_zero_var_groups, void* hip_stream) {
+  Range range("grpo_advantages");
   if (!d_rewards || !d_adv) return fail(nullptr, ROLLOUT_EINVAL, "rewards and advantages must be non-NULL");
   if (n_groups < 1 || group_size < 1) return fail(nullptr, ROLLOUT_EINVAL, "n_groups and group_size must be >= 1");
   if (std_ddof != 0 && std_ddof != 1) return fail(nullptr, ROLLOUT_EINVAL, "std_ddof must be 0 or 1");
@@ -760,6 +817,7 @@ rollout_status grpo_advantages(const float* d_rewards, int32_t n_groups, int32_t
 rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int32_t n_prompts, int32_t prompt_len,
                                 int32_t group_size, int32_t seqs_in_flight, int32_t max_new_tokens, float temperature,
                                 float top_p, const float* d_uniforms, int32_t* d_tokens_out) {
+  Range range("rollout_generate");
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   if (!d_prompts || !d_uniforms || !d_tokens_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
   if (n_prompts < 1 || group_size < 1 || seqs_in_flight < 1)
@@ -770,6 +828,7 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
     return fail(ctx, ROLLOUT_EINVAL, "max_new_tokens must be in [1, config max_new_tokens]");
   if (!(temperature >= 0.f) || !std::isfinite(temperature)) return fail(ctx, ROLLOUT_EINVAL, "temperature must be >= 0");
   if (!(top_p > 0.f && top_p <= 1.f)) return fail(ctx, ROLLOUT_EINVAL, "top_p must be in (0, 1]");
+  reap_graphs(ctx, false);
   const Dims& D = ctx->D;
   // sequences per wave: whole groups, within the context's rows and the KV pool
   int S = std::min<int64_t>(seqs_in_flight, ctx->Lo.S) / group_size * group_size;
@@ -826,18 +885,29 @@ rollout_status rollout_generate(rollout_ctx* ctx, const int32_t* d_prompts, int3
     hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
     hipGraphDestroy(graph);
     if (ie != hipSuccess) return hip_fail(ctx, ie, "graph instantiate");
-    for (int t = 1; t < N; ++t) {
-      hipError_t le = hipGraphLaunch(exec, ctx->stream);
-      if (le != hipSuccess) {
-        hipStreamSynchronize(ctx->stream);
-        hipGraphExecDestroy(exec);
-        return hip_fail(ctx, le, "graph launch");
+    {
+      Range replay("rollout_generate: decode steps (graph replay)");
+      for (int t = 1; t < N; ++t) {
+        hipError_t le = hipGraphLaunch(exec, ctx->stream);
+        if (le != hipSuccess) {
+          hipStreamSynchronize(ctx->stream);
+          hipGraphExecDestroy(exec);
+          return hip_fail(ctx, le, "graph launch");
+        }
+        ctx->cur_len += 1;
       }
-      ctx->cur_len += 1;
     }
-    hipError_t se = hipStreamSynchronize(ctx->stream);
-    hipGraphExecDestroy(exec);
-    if (se != hipSuccess) return hip_fail(ctx, se, "stream sync");
+    // the replays run on after the call returns: the executable is destroyed once they have finished
+    hipEvent_t done = nullptr;
+    hipError_t ee = hipEventCreateWithFlags(&done, hipEventDisableTiming);
+    if (ee == hipSuccess) ee = hipEventRecord(done, ctx->stream);
+    if (ee != hipSuccess) {
+      hipStreamSynchronize(ctx->stream);
+      hipGraphExecDestroy(exec);
+      if (done) hipEventDestroy(done);
+      return hip_fail(ctx, ee, "wave event");
+    }
+    ctx->retired.emplace_back(exec, done);
   }
   return ROLLOUT_OK;
 }
@@ -848,6 +918,7 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
                                     const int32_t* d_stop_ids, int32_t n_stop, int32_t refill_interval,
                                     int32_t whole_groups, int32_t* d_tokens_out, int32_t* d_lengths_out,
                                     int32_t* d_admit_step_out, int32_t* h_decode_steps_out) {
+  Range range("rollout_generate_eos");
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   if (!d_prompts || !d_uniforms || !d_tokens_out || !d_lengths_out) return fail(ctx, ROLLOUT_EINVAL, "NULL buffer");
   if (n_stop < 0 || (n_stop > 0 && !d_stop_ids)) return fail(ctx, ROLLOUT_EINVAL, "n_stop < 0 or stop ids NULL");
@@ -881,6 +952,10 @@ rollout_status rollout_generate_eos(rollout_ctx* ctx, const int32_t* d_prompts, 
     if (S < G) return fail(ctx, ROLLOUT_ENOMEM, "one group does not fit in the context");
     S = std::min(S / G, (int)n_prompts) * G;
   } else {
+    // a group's token-0 prefill and draw write G rows of logits and sampler scratch, sized for the context's rows
+    if (G > Lo.S)
+      return fail(ctx, ROLLOUT_ENOMEM, "group_size " + std::to_string(G) + " exceeds the context's " +
+                                           std::to_string(Lo.S) + " rows (a group's first tokens are drawn together)");
     // single completions: one block-table row beyond the slots serves the prefills; up to S + 1 prompt
     // records are alive at once (a group per occupied slot, plus the one being admitted)
     S = std::min<int64_t>(std::min<int64_t>(seqs_in_flight, Lo.S - 1), n_seq);
@@ -1066,6 +1141,7 @@ rollout_status rollout_sync(rollout_ctx* ctx) {
   if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
   int32_t flag = 0;
   HIP_TRY(ctx, hipStreamSynchronize(ctx->stream), "stream sync");
+  reap_graphs(ctx, true);
   HIP_TRY(ctx, hipMemcpy(&flag, ctx->at(ctx->Lo.err), 4, hipMemcpyDeviceToHost), "error flag read");
   if (flag) {
     HIP_TRY(ctx, hipMemset(ctx->at(ctx->Lo.err), 0, 4), "error flag clear");
@@ -1092,7 +1168,7 @@ rollout_status rollout_export_weight(rollout_ctx* ctx, int32_t tensor_id, float*
   } else if (tensor_id >= 1 && tensor_id < 1 + 9 * D.L) {
     const int l = (tensor_id - 1) / 9, slot = (tensor_id - 1) % 9;
     const Layer& y = Lo.layers[l];
-    // int4 projections export their dequantised (bf16-rounded) values
+    // int4 projections export their dequantised values (q - z) * s, rounded once to fp32
     auto exp = [&](const void* src, const WeightDesc& w, int which, int rows) {
       return D.wq4 ? launch_export_q4(ctx->stream, src, w, which, rows, d_out)
                    : launch_export(ctx->stream, src, D.dtype, w, which, rows, d_out);

@@ -686,6 +686,16 @@ size_t sample_scratch_bytes(int S, int V) {
   return (size_t)S * V * 4 + (size_t)S * nc * (4 + 4 + 8 * 4 + 256 * 8) + (size_t)S * sizeof(RowSel) + 4096;
 }
 
+int sample_rows_fitting(size_t bytes, int V) {
+  const size_t one = sample_scratch_bytes(1, V);
+  if (one > bytes) return 0;
+  const size_t per_row = sample_scratch_bytes(2, V) - one;
+  size_t r = 1 + (bytes - one) / per_row;
+  if (r > (size_t)INT_MAX) r = INT_MAX;
+  while (r > 1 && sample_scratch_bytes((int)r, V) > bytes) --r;
+  return (int)r;
+}
+
 hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float temperature, float top_p,
                          const float* u, int u_stride, const int32_t* col, int32_t* out, int out_stride,
                          void* scratch) {

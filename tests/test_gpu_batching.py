@@ -120,13 +120,39 @@ def test_bf16_eos_schedule_and_stop_rule(refill, slots, whole_groups, P, shared,
     want_admit, want_steps = _expected_schedule(L, G, eff_slots, refill, whole_groups)
     assert list(admit) == list(want_admit) and steps == want_steps
     assert L.min() < N and len(set(L.tolist())) > 3
-    # token 0 of every completion is drawn from its prompt's prefill logits: the same as rollout_generate's
-    out = torch.full((n_prompts * G, N), -1, dtype=torch.int32, device="cuda:0")
-    R.rollout_generate(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, 8, N, 1.0, 1.0, to_dev(u, torch), out)
-    eng.synchronize()
-    same0 = float(np.mean(out.cpu().numpy()[:, 0] == tok[:, 0]))
-    log(f"  token 0 agreement with rollout_generate: {same0:.2f}")
-    assert same0 >= 0.9
+    # token 0 of every completion is drawn from its prompt's prefill logits with u[s, 0]: the admission
+    # prefills one prompt at a time (M = P rows), so the same prefill through rollout_prefill + rollout_sample
+    # runs the same kernels at the same M and must draw the same token, exactly
+    logits = torch.empty((G, cfg.vocab), dtype=torch.float32, device="cuda:0")
+    first = torch.empty(G, dtype=torch.int32, device="cuda:0")
+    want0 = np.empty(n_prompts * G, dtype=np.int32)
+    for p in range(n_prompts):
+        R.rollout_prefill(eng.ctx, to_dev(prompts[p:p + 1], torch), 1, P, G, logits)
+        R.rollout_sample(eng.ctx, logits, G, 1.0, 1.0, to_dev(np.ascontiguousarray(u[p * G:(p + 1) * G, 0]), torch),
+                         first)
+        eng.synchronize()
+        want0[p * G:(p + 1) * G] = first.cpu().numpy()
+    log(f"  token 0 equal to the one-prompt prefill's draw: {int(np.sum(want0 == tok[:, 0]))}/{n_prompts * G}")
+    assert np.array_equal(want0, tok[:, 0])
+    eng.close()
+
+
+def test_single_refill_rejects_groups_wider_than_the_context():
+    # a group's token-0 prefill and draw fill G rows of buffers sized for the context's sequence rows
+    cfg = R.model_config("tiny", R.DTYPE_FP32, 8, 4, 4)
+    eng = R.Engine(cfg, group_size=1)
+    assert eng.cfg.max_seqs_in_flight == 4
+    dev = "cuda:0"
+    G = 8
+    prompts = W.prompts(1, 8, cfg.vocab)
+    u = W.uniforms(G, 4)
+    tokens = torch.empty((G, 4), dtype=torch.int32, device=dev)
+    lengths = torch.empty(G, dtype=torch.int32, device=dev)
+    stop = torch.zeros(1, dtype=torch.int32, device=dev)
+    with pytest.raises(R.RolloutError, match="ENOMEM"):
+        R.rollout_generate_eos(eng.ctx, to_dev(prompts, torch), 1, 8, G, 4, 4, 1.0, 1.0, to_dev(u, torch), stop, 0, 1,
+                               0, tokens, lengths)
+    eng.synchronize()  # nothing was enqueued; the context stays usable
     eng.close()
 
 

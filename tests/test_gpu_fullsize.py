@@ -1,5 +1,5 @@
-"""Full-size parity: one transformer layer at the full width and vocabulary of a benchmark shape, run by the
-GPU in that benchmark's launch configuration, against the oracle on sampled outputs.
+"""Full-size parity: one transformer layer (two at the 7B width) at the full width and vocabulary of a
+benchmark shape, run by the GPU in that benchmark's launch configuration, against the oracle on sampled outputs.
 
 * 7B-class (d 3584, GQA 28/4 x 128, FFN 18944, vocabulary 152064): 8 prompts x 256 tokens, G = 8, 64
   sequences -- prefill at M = 2048 on the tile GEMM, decode at M = 64 on the ring GEMMs and the 4-wave
@@ -30,10 +30,12 @@ torch = pytest.importorskip("torch")
 
 STEPS = 2
 CASES = {
-    # name: (shape, prompts, prompt length, G, prompts compared on the oracle)
-    "7b": (W.ModelShape(1, 3584, 28, 4, 128, 18944, 152064, 1e-6, 1e6), 8, 256, 8, range(8)),
-    "14b": (W.ModelShape(1, 5120, 40, 8, 128, 13824, 152064, 1e-6, 1e6), 16, 512, 16, (0, 5, 10, 15)),
-    "72b": (W.ModelShape(1, 8192, 64, 8, 128, 29568, 152064, 1e-6, 1e6), 8, 512, 8, (0, 4, 7)),
+    # name: (shape name, model shape, prompts, prompt length, G, prompts compared on the oracle)
+    "7b": ("7b", W.ModelShape(1, 3584, 28, 4, 128, 18944, 152064, 1e-6, 1e6), 8, 256, 8, range(8)),
+    # two layers: the residual add + RMSNorm between layers (fp32 residual, bf16 normed operand) at full width
+    "7b-2layers": ("7b", W.ModelShape(2, 3584, 28, 4, 128, 18944, 152064, 1e-6, 1e6), 8, 256, 8, (0, 3, 6)),
+    "14b": ("14b", W.ModelShape(1, 5120, 40, 8, 128, 13824, 152064, 1e-6, 1e6), 16, 512, 16, (0, 5, 10, 15)),
+    "72b": ("72b", W.ModelShape(1, 8192, 64, 8, 128, 29568, 152064, 1e-6, 1e6), 8, 512, 8, (0, 4, 7)),
 }
 
 
@@ -44,13 +46,15 @@ def _oracle(shape, token_ids, vocab_ids):
     w = {"embed": W.weight_rows(0, W.tensor_id_embed(), ids, d),
          "lm_head": W.weight_rows(0, W.tensor_id_lm_head(shape), vocab_ids, d),
          "final_norm": np.ones(d, dtype=np.float32)}
-    lw = {"attn_norm": np.ones(d, np.float32), "mlp_norm": np.ones(d, np.float32)}
-    for slot, name in enumerate(W.LAYER_SLOTS):
-        if name.endswith("norm"):
-            continue
-        lw[name] = W.weight_matrix(0, W.tensor_id_layer(0, slot), *W.logical_shape(shape, name))
-        log(f"  oracle weight {name} {lw[name].shape} generated")
-    w["layers"] = {0: lw}
+    w["layers"] = {}
+    for layer in range(shape.n_layers):
+        lw = {"attn_norm": np.ones(d, np.float32), "mlp_norm": np.ones(d, np.float32)}
+        for slot, name in enumerate(W.LAYER_SLOTS):
+            if name.endswith("norm"):
+                continue
+            lw[name] = W.weight_matrix(0, W.tensor_id_layer(layer, slot), *W.logical_shape(shape, name))
+            log(f"  oracle weight layer {layer} {name} {lw[name].shape} generated")
+        w["layers"][layer] = lw
     log("  oracle weights generated")
     model = OracleModel(shape, w, mode="bf16")
     to_local = np.vectorize(lambda t: remap[int(t)])
@@ -61,16 +65,16 @@ def _oracle(shape, token_ids, vocab_ids):
 def test_full_width_layer_in_the_benchmark_launch_configuration(case, monkeypatch):
     monkeypatch.delenv("ROLLOUT_SHARED_PREFIX", raising=False)
     monkeypatch.delenv("ROLLOUT_ATTN_WAVES", raising=False)
-    shape, n_prompts, P, G, compared = CASES[case]
+    name, shape, n_prompts, P, G, compared = CASES[case]
     S = n_prompts * G
-    log(f"full-size parity, {case}: one layer at full width, {n_prompts} prompts x {P}, G={G}, {S} sequences, "
-        f"prefill + {STEPS} decode steps")
+    log(f"full-size parity, {case}: {shape.n_layers} layer(s) at full width, {n_prompts} prompts x {P}, G={G}, "
+        f"{S} sequences, prefill + {STEPS} decode steps")
     rng = np.random.default_rng(11)
     prompts = W.prompts(n_prompts, P, shape.vocab, seed=71)
     feed = W.prompts(STEPS, S, shape.vocab, seed=72)  # teacher-forced decode tokens [step, sequence]
     vocab_ids = np.sort(rng.choice(shape.vocab, size=4096, replace=False))
     dev = "cuda:0"
-    cfg = R.model_config(case, R.DTYPE_BF16, P, 8, S, n_layers=1)
+    cfg = R.model_config(name, R.DTYPE_BF16, P, 8, S, n_layers=shape.n_layers)
     eng = R.Engine(cfg, group_size=G)
     cols = torch.from_numpy(vocab_ids).to(dev)
     logits = torch.empty((S, shape.vocab), dtype=torch.float32, device=dev)
