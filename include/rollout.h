@@ -257,6 +257,31 @@ void rollout_destroy(rollout_ctx* ctx);
 const char* rollout_last_error(const rollout_ctx* ctx);
 
 /* ------------------------------------------------------------------------ */
+/* Allocation-free draw                                                      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the draw of
+ * rollout_sample without a context.  Same definition and arguments as
+ * rollout_sample, plus the row width vocab and hip_stream (a hipStream_t of
+ * the current device; NULL = its default stream); enqueued on that stream.
+ * Nothing is allocated: the sampler kernels' scratch is one fixed device array
+ * of ROLLOUT_SAMPLE_NOALLOC_SCRATCH_BYTES, held on every GPU the call runs on
+ * until the process ends, and rows are drawn in batches that fit it.  Every
+ * call on a GPU shares that GPU's array, so calls that overlap on one GPU
+ * (several streams or threads) race on it and must be serialised by the
+ * caller.  Errors (message from rollout_last_error(NULL)): EINVAL (NULL
+ * buffer, n_seqs < 1, vocab < 2, temperature < 0, top_p outside (0, 1], a
+ * stream of another device), ENOMEM (one row needs more scratch than the
+ * array holds: vocab above 16,742,770), EDEVICE.
+ */
+#define ROLLOUT_SAMPLE_NOALLOC_SCRATCH_BYTES (64ull << 20)
+rollout_status rollout_sample_noalloc(const float* d_logits, int32_t n_seqs, int32_t vocab, float temperature,
+                                      float top_p, const float* d_uniforms, int32_t* d_tokens_out,
+                                      void* hip_stream);
+
+/* ------------------------------------------------------------------------ */
 /* Inspection and measurement                                                */
 /* ------------------------------------------------------------------------ */
 

@@ -26,7 +26,9 @@ EXPORTED = (
     "rollout_plan", "rollout_init", "rollout_prefill", "rollout_decode_step", "rollout_sample",
     "grpo_advantages", "rollout_generate", "rollout_sync", "rollout_destroy", "rollout_last_error",
     "rollout_export_weight", "rollout_profile_decode_step", "rollout_generate_eos", "rollout_length_rewards",
+    "rollout_sample_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 64 << 20  # ROLLOUT_SAMPLE_NOALLOC_SCRATCH_BYTES
 # include/occupancy.h: power metrics and threshold policy of the occupancy controller (host code)
 EXPORTED_OCC = (
     "occ_rolling_mean", "occ_violation", "occ_normalize_budget", "occ_hysteresis_step", "occ_monitor_create",
@@ -101,6 +103,7 @@ def _load():
         "rollout_generate_eos": ([vp, vp, i32, i32, i32, i32, i32, f32, f32, vp, vp, i32, i32, i32, vp, vp, vp,
                                   ctypes.POINTER(i32)], i32),
         "rollout_length_rewards": ([vp, i32, i32, vp, vp, vp], i32),
+        "rollout_sample_noalloc": ([vp, i32, i32, f32, f32, vp, vp, vp], i32),
         "occ_rolling_mean": ([vp, ctypes.c_int64, f64, f64, vp], i32),
         "occ_violation": ([vp, ctypes.c_int64, f64, f64, ctypes.POINTER(f64), ctypes.POINTER(f64)], i32),
         "occ_normalize_budget": ([f64, f64, f64], f64),
@@ -160,6 +163,12 @@ def rollout_decode_step(ctx, tokens, logits):
 
 def rollout_sample(ctx, logits, n_seqs: int, temperature: float, top_p: float, uniforms, tokens_out):
     _check(lib.rollout_sample(ctx, _ptr(logits), n_seqs, temperature, top_p, _ptr(uniforms), _ptr(tokens_out)), ctx)
+
+
+def rollout_sample_noalloc(logits, n_seqs: int, vocab: int, temperature: float, top_p: float, uniforms, tokens_out,
+                           stream=None):
+    _check(lib.rollout_sample_noalloc(_ptr(logits), n_seqs, vocab, temperature, top_p, _ptr(uniforms),
+                                      _ptr(tokens_out), _ptr(stream)))
 
 
 def grpo_advantages(rewards, n_groups: int, group_size: int, eps: float, std_ddof: int, adv, zero_var=None,

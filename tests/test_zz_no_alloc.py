@@ -1,0 +1,67 @@
+"""rollout_sample_noalloc, the allocation-free draw: the same tokens as rollout_sample, the entry point it is a
+variant of, on the same logits and uniforms -- bit for bit (both decide in exact integers) -- on two calls in
+a row, the second with fewer rows; rows beyond one batch of the fixed scratch; and argument validation that
+happens before any device work."""
+import numpy as np
+import pytest
+
+import paper_2608_11226_amd as R
+import workload as W
+
+torch = pytest.importorskip("torch")
+
+
+def _draw_both(V, S, T, top_p, seed):
+    rng = np.random.default_rng(seed)
+    z = (rng.standard_normal((S, V)) * 2.0).astype(np.float32)
+    z[: min(S, 4)] = np.round(z[: min(S, 4)], 1)  # ties in value
+    u = W.uniforms(S, 1, seed=seed + 1)[:, 0]
+    dev = "cuda:0"
+    zl = torch.from_numpy(z).to(dev)
+    ud = torch.from_numpy(u).to(dev)
+    cfg = R.model_config("tiny", R.DTYPE_FP32, 16, 8, 4)
+    cfg.vocab = V  # rollout_sample takes the row width from its context
+    eng = R.Engine(cfg)
+    want = torch.full((S,), -1, dtype=torch.int32, device=dev)
+    R.rollout_sample(eng.ctx, zl, S, T, top_p, ud, want)
+    eng.synchronize()
+    got = torch.full((S,), -1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream(device=dev)
+    R.rollout_sample_noalloc(zl, S, V, T, top_p, ud, got, stream.cuda_stream)
+    stream.synchronize()
+    eng.close()
+    return got.cpu().numpy(), want.cpu().numpy()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("V,T,top_p", [(152064, 0.9, 0.95), (152064, 1.0, 1.0), (152064, 0.0, 1.0), (2048, 0.7, 0.5)])
+def test_noalloc_draw_equals_rollout_sample_twice_the_second_smaller(V, T, top_p):
+    print(f"noalloc sampler V={V} T={T} top_p={top_p}: 64 rows then 16", flush=True)
+    for S, seed in ((64, 3), (16, 7)):
+        got, want = _draw_both(V, S, T, top_p, seed)
+        assert np.all((want >= 0) & (want < V))
+        assert np.array_equal(got, want), np.nonzero(got != want)
+
+
+@pytest.mark.gpu
+def test_noalloc_draw_in_several_batches_of_the_fixed_scratch():
+    # 152064 logits per row: the 64 MiB scratch holds 97 rows, so 200 rows take three batches
+    V, S = 152064, 200
+    per_row = 4 * V + 38 * 2088 + 56
+    assert (R.NOALLOC_SCRATCH_BYTES - 4096) // per_row < S
+    print(f"noalloc sampler V={V}: {S} rows in batches", flush=True)
+    got, want = _draw_both(V, S, 0.9, 0.95, 11)
+    assert np.array_equal(got, want), np.nonzero(got != want)
+
+
+def test_noalloc_validates_before_any_device_work():
+    # fake (never dereferenced) addresses: every error below is raised before the device is touched
+    fake = 1 << 20
+    with pytest.raises(R.RolloutError, match="ENOMEM"):
+        R.rollout_sample_noalloc(fake, 1, 16_742_771, 1.0, 1.0, fake, fake)
+    for args in ((0, 1, 1024, 1.0, 1.0, fake, fake), (fake, 0, 1024, 1.0, 1.0, fake, fake),
+                 (fake, 1, 1, 1.0, 1.0, fake, fake), (fake, 1, 1024, -1.0, 1.0, fake, fake),
+                 (fake, 1, 1024, 1.0, 0.0, fake, fake), (fake, 1, 1024, 1.0, 1.5, fake, fake)):
+        with pytest.raises(R.RolloutError, match="EINVAL"):
+            R.rollout_sample_noalloc(*args)
+    assert "top_p" in R.rollout_last_error()
