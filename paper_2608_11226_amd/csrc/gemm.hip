@@ -27,6 +27,9 @@
 // that holds one also holds the other, and h goes straight to the down
 // projection's operand layout.
 //
+// Gate/up with SwiGLU at decode batches whose weight blocks give every CU 4 to 10 of them (7B) takes a
+// balanced grid instead: one workgroup of two waves per CU, the blocks shared out evenly (BAL below).
+//
 // k_gemm_tile (prefill and other batches above 64 rows): a workgroup of four
 // waves owns 256 weight rows x 128 activation rows; each wave owns its own 64
 // weight rows against all 128 activation rows (4 x 8 MFMA tiles, 128
@@ -195,14 +198,25 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
 // MB = ceil(M/16) row blocks of X; NBW weight blocks per wave; D ring stages; KW waves per workgroup, which
 // split the workgroup's K slice between them and add their sums through LDS (in wave order) before the
 // epilogue, so a workgroup writes one partial however many waves it has.
-template <int MB, int NBW, int D, bool SWI, int KW>
+// BAL: the grid's workgroups share the N/16 weight blocks out evenly, floor(nbt / grid) or one more each
+// (at most NBW), so that a grid of one workgroup per CU gives every CU the same work; otherwise workgroup x
+// owns blocks NBW x .. NBW x + NBW - 1.  A workgroup with fewer than NBW blocks loads its last block again
+// for the missing ones (a cache hit) and stores nothing for them.
+template <int MB, int NBW, int D, bool SWI, int KW, bool BAL = false>
 __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W,
                                                        float* __restrict__ out, int M, int N, int K, int kslice,
                                                        uint16_t* __restrict__ h) {
   const int lane = threadIdx.x & 63;
   const int wave = KW > 1 ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) : 0;
-  const int nb0 = blockIdx.x * NBW;
   const int nbt = N >> 4, kbt = K >> 5;
+  int nb0, nbc;  // the workgroup's first weight block and its block count (>= 1)
+  if constexpr (BAL) {
+    nb0 = (int)((long long)blockIdx.x * nbt / gridDim.x);
+    nbc = (int)((long long)(blockIdx.x + 1) * nbt / gridDim.x) - nb0;
+  } else {
+    nb0 = blockIdx.x * NBW;
+    nbc = min(NBW, nbt - nb0);
+  }
   const int kw0 = (int)blockIdx.y * (kslice >> 5);         // the workgroup's first k-step
   const int nkw = min(kbt, kw0 + (kslice >> 5)) - kw0;    // and its k-steps (none in a surplus split)
   const int per = (nkw + KW - 1) / KW;
@@ -211,7 +225,7 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
   if constexpr (KW == 1) {
     if (nk <= 0) {  // an empty K split contributes zeros
       if constexpr (!SWI) {
-        for (int j = 0; j < NBW && nb0 + j < nbt; ++j)
+        for (int j = 0; j < nbc; ++j)
           for (int m = lane & 15; m < M; m += 16)
             *reinterpret_cast<float4*>(out + ((size_t)blockIdx.y * M + m) * N + (nb0 + j) * 16 + 4 * (lane >> 4)) =
                 make_float4(0.f, 0.f, 0.f, 0.f);
@@ -229,7 +243,7 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
     int ws[NBW];  // k-step stride of each block's fragments
 #pragma unroll
     for (int j = 0; j < NBW; ++j) {
-      const int nb = min(nb0 + j, nbt - 1);
+      const int nb = nb0 + min(j, nbc - 1);
       wp[j] = W + wfrag(nb, kb0, nbt, kbt) * 64 + lane;
       ws[j] = wgroup_blocks(nb, nbt) * 64;
     }
@@ -296,7 +310,7 @@ __global__ __launch_bounds__(64 * KW) void k_gemm_ring(const bf16x8_t* __restric
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
-    if (j % KW != wave || nb0 + j >= nbt) continue;
+    if (j % KW != wave || j >= nbc) continue;
     const int n = (nb0 + j) * 16 + 4 * (lane >> 4);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -560,6 +574,43 @@ void launch_ring_kw(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* 
   }
 }
 
+// Compute units of the current device (looked up once per device).
+int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+// Gate/up with SwiGLU at decode batches, balanced: one workgroup of two waves per CU (the two waves split
+// K and add their sums through LDS), the weight blocks shared out evenly, floor(nbt / CUs) or one more per
+// workgroup.  The one-wave-per-four-blocks grid (7B: 592 waves) leaves 80 CUs with three waves and 176
+// with two, and a CU's streaming rate, not HBM, bounds these kernels: the CUs with three waves set the
+// time (7B gate/up 52.8 -> 50.0 us in isolation).  Taken when every CU gets between 4 and kBalNBW blocks.
+constexpr int kBalNBW = 10;
+bool use_balanced_swiglu(int M, int N) {
+  const int nbt = N / 16, cus = device_cus();
+  return M <= kRingMaxRows && nbt >= 4 * cus && nbt <= kBalNBW * cus;
+}
+
+hipError_t launch_ring_balanced_swiglu(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, int M, int N, int K,
+                                       uint16_t* h) {
+  const int kslice = kslice_for(K, 1);
+  const dim3 grid(device_cus(), 1), block(128);
+  switch ((M + 15) / 16) {
+    case 1: hipLaunchKernelGGL((k_gemm_ring<1, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
+    case 2: hipLaunchKernelGGL((k_gemm_ring<2, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
+    case 3: hipLaunchKernelGGL((k_gemm_ring<3, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
+    default: hipLaunchKernelGGL((k_gemm_ring<4, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
+  }
+  return hipGetLastError();
+}
+
 template <int NBW, bool SWI>
 hipError_t launch_ring(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
                        int splits, uint16_t* h) {
@@ -677,6 +728,8 @@ hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M
                              (uint16_t*)h);
     return hipGetLastError();
   }
+  if (use_balanced_swiglu(M, N))
+    return launch_ring_balanced_swiglu(s, (const bf16x8_t*)X, (const bf16x8_t*)W, M, N, K, (uint16_t*)h);
   return launch_ring<4, true>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, 1, (uint16_t*)h);
 }
 

@@ -330,7 +330,10 @@ def test_bf16_gqa7_large_batch_teacher_forced_logits(monkeypatch):
 # the second wave of a two-wave decode workgroup has none), d_model 96 / d_ff 160 (3 and 5 k-steps, split
 # unevenly between the two waves), and row counts (QKV 160 = 10 blocks, vocab 208 = 13 blocks) that leave
 # the last four-block weight group short.  Prefill (72 rows) takes the tile GEMM, decode the ring.
-ODD_BF16 = [(1, 32, 1, 1, 32, 32, 64, 1e4), (2, 96, 3, 1, 32, 160, 208, 1e4)]
+ODD_BF16 = [(1, 32, 1, 1, 32, 32, 64, 1e4), (2, 96, 3, 1, 32, 160, 208, 1e4),
+            # gate/up of 2 x 9248 rows = 1156 blocks: the balanced decode grid (one workgroup per CU, 4 or 5
+            # blocks each, the two waves splitting K)
+            (1, 128, 4, 2, 32, 9248, 512, 1e4)]
 
 
 @pytest.mark.parametrize("shape", ODD_BF16)
