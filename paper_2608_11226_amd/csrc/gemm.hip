@@ -28,7 +28,8 @@
 // projection's operand layout.
 //
 // Gate/up with SwiGLU at decode batches whose weight blocks give every CU 4 to 10 of them (7B) takes a
-// balanced grid instead: one workgroup of two waves per CU, the blocks shared out evenly (BAL below).
+// balanced grid instead: one workgroup of two waves per CU, the blocks shared out evenly (BAL below); so
+// does the LM head, with four one-wave workgroups per CU.
 //
 // k_gemm_tile (prefill and other batches above 64 rows): a workgroup of four
 // waves owns 256 weight rows x 128 activation rows; each wave owns its own 64
@@ -592,21 +593,30 @@ int device_cus() {
 // workgroup.  The one-wave-per-four-blocks grid (7B: 592 waves) leaves 80 CUs with three waves and 176
 // with two, and a CU's streaming rate, not HBM, bounds these kernels: the CUs with three waves set the
 // time (7B gate/up 52.8 -> 50.0 us in isolation).  Taken when every CU gets between 4 and kBalNBW blocks.
+// The same balance for single-split projections of many blocks (the LM head): four one-wave workgroups per
+// CU, each with floor(nbt / grid) or one more of the blocks (7B: 9 or 10 instead of 1188 eight-block
+// workgroups, 4.6 per CU; LM head 199.7 -> 180.4 us in isolation).
 constexpr int kBalNBW = 10;
+constexpr int kBalWavesPerCU = 4;
 bool use_balanced_swiglu(int M, int N) {
   const int nbt = N / 16, cus = device_cus();
   return M <= kRingMaxRows && nbt >= 4 * cus && nbt <= kBalNBW * cus;
 }
+bool use_balanced_single(int M, int N, int splits) {
+  const int nbt = N / 16, g = kBalWavesPerCU * device_cus();
+  return M <= kRingMaxRows && splits == 1 && nbt >= 4 * g && nbt <= kBalNBW * g;
+}
 
-hipError_t launch_ring_balanced_swiglu(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, int M, int N, int K,
-                                       uint16_t* h) {
+template <bool SWI, int KW>
+hipError_t launch_ring_balanced(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
+                                int groups, uint16_t* h) {
   const int kslice = kslice_for(K, 1);
-  const dim3 grid(device_cus(), 1), block(128);
+  const dim3 grid(groups, 1), block(64 * KW);
   switch ((M + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_gemm_ring<1, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
-    case 2: hipLaunchKernelGGL((k_gemm_ring<2, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
-    case 3: hipLaunchKernelGGL((k_gemm_ring<3, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
-    default: hipLaunchKernelGGL((k_gemm_ring<4, kBalNBW, 2, true, 2, true>), grid, block, 0, s, x, w, nullptr, M, N, K, kslice, h); break;
+    case 1: hipLaunchKernelGGL((k_gemm_ring<1, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 2: hipLaunchKernelGGL((k_gemm_ring<2, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 3: hipLaunchKernelGGL((k_gemm_ring<3, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    default: hipLaunchKernelGGL((k_gemm_ring<4, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
   }
   return hipGetLastError();
 }
@@ -715,7 +725,11 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
   if (N % 16 || K % 32) return hipErrorInvalidValue;
   const bf16x8_t* x = (const bf16x8_t*)X;
   const bf16x8_t* w = (const bf16x8_t*)W;
-  if (M <= kRingMaxRows) return launch_ring<8, false>(s, x, w, out, M, N, K, splits, nullptr);
+  if (M <= kRingMaxRows) {
+    if (use_balanced_single(M, N, splits))
+      return launch_ring_balanced<false, 1>(s, x, w, out, M, N, K, kBalWavesPerCU * device_cus(), nullptr);
+    return launch_ring<8, false>(s, x, w, out, M, N, K, splits, nullptr);
+  }
   return launch_tile(s, x, w, out, M, N, K, splits);
 }
 
@@ -729,7 +743,8 @@ hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M
     return hipGetLastError();
   }
   if (use_balanced_swiglu(M, N))
-    return launch_ring_balanced_swiglu(s, (const bf16x8_t*)X, (const bf16x8_t*)W, M, N, K, (uint16_t*)h);
+    return launch_ring_balanced<true, 2>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, device_cus(),
+                                         (uint16_t*)h);
   return launch_ring<4, true>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, 1, (uint16_t*)h);
 }
 

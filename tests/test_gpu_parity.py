@@ -332,8 +332,9 @@ def test_bf16_gqa7_large_batch_teacher_forced_logits(monkeypatch):
 # the last four-block weight group short.  Prefill (72 rows) takes the tile GEMM, decode the ring.
 ODD_BF16 = [(1, 32, 1, 1, 32, 32, 64, 1e4), (2, 96, 3, 1, 32, 160, 208, 1e4),
             # gate/up of 2 x 9248 rows = 1156 blocks: the balanced decode grid (one workgroup per CU, 4 or 5
-            # blocks each, the two waves splitting K)
-            (1, 128, 4, 2, 32, 9248, 512, 1e4)]
+            # blocks each, the two waves splitting K); a vocabulary of 75,008 = 4688 blocks: the balanced LM
+            # head (four one-wave workgroups per CU, 4 or 5 blocks each)
+            (1, 128, 4, 2, 32, 9248, 75008, 1e4)]
 
 
 @pytest.mark.parametrize("shape", ODD_BF16)
