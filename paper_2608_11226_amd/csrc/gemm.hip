@@ -71,68 +71,85 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-// Tile kernel: 4 waves, 256 weight rows x 128 activation rows per workgroup, each wave 64 x 128.
-constexpr int kTileNB = 4;            // 16-row weight blocks per wave
-constexpr int kTileMB = 8;            // 16-row activation blocks per workgroup
+// Tile kernel: 4 waves; a workgroup owns NB 16-row weight blocks per wave against MBW 16-row activation
+// blocks.  Prefill: NB = 4, MBW = 8 (256 weight rows x 128 activation rows, each wave 64 x 128).  Tall
+// decode batches (129..256 rows): NB = 2, MBW = 16 (128 weight rows x all 256 activation rows), so every
+// weight byte is streamed into one CU only, not once per 128-row activation tile.
 constexpr int kTileWaves = 4;
-constexpr int kTileXPW = kTileMB / kTileWaves;  // activation fragments each wave stages per k-step
+constexpr int kTileNB = 4, kTileMB = 8;  // prefill shape
+constexpr int kTallNB = 2, kTallMB = 16; // tall decode shape
 
 // SWI: gate/up with SwiGLU applied to the output (one K split): h in the down projection's operand layout
 // XD: activation register stages (each k-step's X fragments are loaded XD steps before they are staged
 // into LDS); OCC: waves per SIMD the registers are sized for.  Batches above 256 rows (prefill, MFMA-bound)
 // take XD = 3 at two waves per SIMD; decode-sized batches, one wave per SIMD anyway, take XD = 6.
-template <bool SWI, int XD, int OCC>
+// BAL (one activation tile): the grid's workgroups share the weight blocks out evenly, floor(nbt / grid) or
+// one more each (at most NB * 4); wave w takes the workgroup's blocks NB w .. NB w + NB - 1, and a wave
+// with fewer (or none) loads the workgroup's last block again for them and stores nothing for them.
+// Otherwise workgroups run in XCD-aware order: the M tiles of one N tile share one XCD and its L2.
+template <int NB, int MBW, bool SWI, int XD, int OCC, bool BAL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W, float* __restrict__ out,
                  int M, int N, int K, int kslice, uint16_t* __restrict__ h) {
-  __shared__ bf16x8_t xs[2][kTileMB][64];
+  constexpr int XPW = MBW / kTileWaves;  // activation fragments each wave stages per k-step
+  __shared__ bf16x8_t xs[2][MBW][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nbt = N >> 4, kbt = K >> 5, Mb = (M + 15) >> 4;
-  const int Mt = (Mb + kTileMB - 1) / kTileMB, Nt = (nbt + kTileNB * kTileWaves - 1) / (kTileNB * kTileWaves);
-  // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD and its L2
-  const int b = blockIdx.x;
-  const int grp = b / (8 * Mt), rem = b % (8 * Mt);
-  const int nt = grp * 8 + rem % 8, mt = rem / 8;
-  if (nt >= Nt) return;
-  const int nb0 = nt * kTileNB * kTileWaves + wave * kTileNB, mb0 = mt * kTileMB;
+  int wb0, wbc, mb0;  // the workgroup's first weight block, its block count and its first activation block
+  if constexpr (BAL) {
+    wb0 = (int)((long long)blockIdx.x * nbt / gridDim.x);
+    wbc = (int)((long long)(blockIdx.x + 1) * nbt / gridDim.x) - wb0;
+    mb0 = 0;
+  } else {
+    const int Mt = (Mb + MBW - 1) / MBW, Nt = (nbt + NB * kTileWaves - 1) / (NB * kTileWaves);
+    // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD and its L2
+    const int b = blockIdx.x;
+    const int grp = b / (8 * Mt), rem = b % (8 * Mt);
+    const int nt = grp * 8 + rem % 8, mt = rem / 8;
+    if (nt >= Nt) return;
+    wb0 = nt * NB * kTileWaves;
+    wbc = min(NB * kTileWaves, nbt - wb0);
+    mb0 = mt * MBW;
+  }
+  const int lb0 = wave * NB;  // the wave's first block within the workgroup's
   const int kb0 = (int)blockIdx.y * (kslice >> 5);
   const int nk = min(kbt, kb0 + (kslice >> 5)) - kb0;
-  floatx4_t acc[kTileNB][kTileMB];
+  floatx4_t acc[NB][MBW];
 #pragma unroll
-  for (int j = 0; j < kTileNB; ++j)
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
-    for (int i = 0; i < kTileMB; ++i) acc[j][i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < MBW; ++i) acc[j][i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   if (nk > 0) {
     // every load is unconditional: block and k indices are clamped into range, surplus k-steps are not computed
-    const bf16x8_t* wp[kTileNB];
-    int ws[kTileNB];  // k-step stride of each block's fragments
+    const bf16x8_t* wp[NB];
+    int ws[NB];  // k-step stride of each block's fragments
 #pragma unroll
-    for (int j = 0; j < kTileNB; ++j) {
-      const int nb = min(nb0 + j, nbt - 1);
+    for (int j = 0; j < NB; ++j) {
+      const int nb = wb0 + min(lb0 + j, wbc - 1);
       wp[j] = W + wfrag(nb, kb0, nbt, kbt) * 64 + lane;
       ws[j] = wgroup_blocks(nb, nbt) * 64;
     }
-    const bf16x8_t* xp[kTileXPW];
+    const bf16x8_t* xp[XPW];
 #pragma unroll
-    for (int i = 0; i < kTileXPW; ++i)
-      xp[i] = XF + ((size_t)kb0 * Mb + min(mb0 + kTileXPW * wave + i, Mb - 1)) * 64 + lane;
+    for (int i = 0; i < XPW; ++i)
+      xp[i] = XF + ((size_t)kb0 * Mb + min(mb0 + XPW * wave + i, Mb - 1)) * 64 + lane;
     const size_t xstride = (size_t)Mb * 64;
     static_assert(6 % XD == 0, "the k-step loop is unrolled by 6");
-    bf16x8_t wr[3][kTileNB], xg[XD][kTileXPW];
+    bf16x8_t wr[3][NB], xg[XD][XPW];
     auto load_w = [&](int slot, int st) {
       const size_t kk = (size_t)min(st, nk - 1);
 #pragma unroll
-      for (int j = 0; j < kTileNB; ++j) wr[slot][j] = wp[j][kk * ws[j]];
+      for (int j = 0; j < NB; ++j) wr[slot][j] = wp[j][kk * ws[j]];
     };
     auto load_x = [&](int slot, int st) {
       const size_t kk = (size_t)min(st, nk - 1);
 #pragma unroll
-      for (int i = 0; i < kTileXPW; ++i) xg[slot][i] = xp[i][kk * xstride];
+      for (int i = 0; i < XPW; ++i) xg[slot][i] = xp[i][kk * xstride];
     };
     auto stage_x = [&](int buf, int slot) {
 #pragma unroll
-      for (int i = 0; i < kTileXPW; ++i) xs[buf][kTileXPW * wave + i][lane] = xg[slot][i];
+      for (int i = 0; i < XPW; ++i) xs[buf][XPW * wave + i][lane] = xg[slot][i];
     };
     // k-step st computes from LDS buffer st % 2 and weight slot st % 3.  Before it, the step loads
     // W(st + 2), writes X(st + 1) (loaded XD steps earlier, register slot (st + 1) % XD) into the other LDS
@@ -154,20 +171,20 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
         load_x((u + 1) % XD, st + 1 + XD);
         if (st < nk) {
 #pragma unroll
-          for (int i = 0; i < kTileMB; ++i) {
+          for (int i = 0; i < MBW; ++i) {
             const bf16x8_t xf = xs[u & 1][i][lane];
 #pragma unroll
-            for (int j = 0; j < kTileNB; ++j)
+            for (int j = 0; j < NB; ++j)
               acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wr[u % 3][j], xf, acc[j][i], 0, 0, 0);
           }
-          // two LDS fragment reads ahead of the MFMAs, then one more per group of four
+          // two LDS fragment reads ahead of the MFMAs, then one more per fragment's NB MFMAs
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-          for (int i = 0; i < kTileMB - 2; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+          for (int i = 0; i < MBW - 2; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, NB, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
         }
         lds_barrier();
       }
@@ -176,12 +193,11 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
   // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
   float* o = out + (size_t)blockIdx.y * M * N;
 #pragma unroll
-  for (int j = 0; j < kTileNB; ++j) {
-    const int nb = nb0 + j;
-    if (nb >= nbt) continue;
-    const int n = nb * 16 + 4 * (lane >> 4);
+  for (int j = 0; j < NB; ++j) {
+    if (lb0 + j >= wbc) continue;
+    const int n = (wb0 + lb0 + j) * 16 + 4 * (lane >> 4);
 #pragma unroll
-    for (int i = 0; i < kTileMB; ++i) {
+    for (int i = 0; i < MBW; ++i) {
       const int m = (mb0 + i) * 16 + (lane & 15);
       if (m >= M) continue;
       if constexpr (SWI) {
@@ -516,28 +532,59 @@ int kslice_for(int K, int splits) {
   return (per + 31) / 32 * 32;
 }
 
+// Compute units of the current device (looked up once per device).
+int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 // Tile kernel grid: (padded N tiles) x (M tiles) workgroups in XCD-aware order, K splits in y.
 int tile_m_tiles(int M) { return ((M + 15) / 16 + kTileMB - 1) / kTileMB; }
 int tile_n_tiles(int N) { return (N / 16 + kTileNB * kTileWaves - 1) / (kTileNB * kTileWaves); }
 int tile_groups(int M, int N) { return (tile_n_tiles(N) + 7) / 8 * 8 * tile_m_tiles(M); }
+
+// Tall decode batches (129..256 rows, one activation tile): balanced grid of workgroups with at most
+// kTallNB * 4 weight blocks each, about one per CU per K split.
+constexpr int kTallMinRows = 129, kTallMaxRows = 256;
+constexpr int kTallWgBlocks = kTallNB * kTileWaves;
+bool tall_batch(int M) { return M >= kTallMinRows && M <= kTallMaxRows; }
+int tall_groups(int N, int splits) {
+  const int nbt = N / 16;
+  const int need = (nbt + kTallWgBlocks - 1) / kTallWgBlocks;
+  return std::min(nbt, std::max(need, device_cus() / splits));
+}
 
 // Decode-sized batches (at most kTileDecodeRows rows) run one wave per SIMD whatever the register budget, so
 // they take the deeper activation staging (14B at 256 rows: QKV -6%, O -8%, gate/up -3.5%); prefill keeps
 // two waves per SIMD with three stages (7B prefill gate/up -3% against two).
 constexpr int kTileDecodeRows = 256;
 template <bool SWI>
-void launch_tile_kernel(hipStream_t s, dim3 grid, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
-                        int kslice, uint16_t* h) {
-  if (M <= kTileDecodeRows)
-    hipLaunchKernelGGL((k_gemm_tile<SWI, 6, 1>), grid, dim3(64 * kTileWaves), 0, s, x, w, out, M, N, K, kslice, h);
-  else
-    hipLaunchKernelGGL((k_gemm_tile<SWI, 3, 2>), grid, dim3(64 * kTileWaves), 0, s, x, w, out, M, N, K, kslice, h);
+void launch_tile_kernel(hipStream_t s, int splits, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N,
+                        int K, uint16_t* h) {
+  const int kslice = kslice_for(K, splits);
+  const dim3 block(64 * kTileWaves);
+  if (tall_batch(M)) {
+    const dim3 grid(tall_groups(N, splits), splits);
+    hipLaunchKernelGGL((k_gemm_tile<kTallNB, kTallMB, SWI, 6, 1, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+  } else if (M <= kTileDecodeRows) {
+    const dim3 grid(tile_groups(M, N), splits);
+    hipLaunchKernelGGL((k_gemm_tile<kTileNB, kTileMB, SWI, 6, 1, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+  } else {
+    const dim3 grid(tile_groups(M, N), splits);
+    hipLaunchKernelGGL((k_gemm_tile<kTileNB, kTileMB, SWI, 3, 2, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+  }
 }
 
 hipError_t launch_tile(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
                        int splits) {
-  const dim3 grid(tile_groups(M, N), splits);
-  launch_tile_kernel<false>(s, grid, x, w, out, M, N, K, kslice_for(K, splits), nullptr);
+  launch_tile_kernel<false>(s, splits, x, w, out, M, N, K, nullptr);
   return hipGetLastError();
 }
 
@@ -573,19 +620,6 @@ void launch_ring_kw(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* 
     case 3: hipLaunchKernelGGL((k_gemm_ring<3, NBW, 2, SWI, KW>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
     default: hipLaunchKernelGGL((k_gemm_ring<4, NBW, 2, SWI, KW>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
   }
-}
-
-// Compute units of the current device (looked up once per device).
-int device_cus() {
-  static int cached[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (!cached[dev]) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
-  }
-  return cached[dev];
 }
 
 // Gate/up with SwiGLU at decode batches, balanced: one workgroup of two waves per CU (the two waves split
@@ -695,7 +729,12 @@ int gemm_splits(int dtype, int M, int N, int K, int max_splits) {
   if (M <= kRingMaxRows) return ring_splits(N, K, max_splits);
   const int nwg = tile_m_tiles(M) * tile_n_tiles(N);
   int s;
-  if (M <= 256) {
+  if (tall_batch(M)) {
+    // one activation tile: K splits until the 128-row weight tiles of all splits fill the 256 CUs once
+    // (a partial costs M x N x 4 bytes, so no more than that)
+    const int tiles = (N / 16 + kTallWgBlocks - 1) / kTallWgBlocks;
+    s = std::max(1, std::min(std::min(max_splits, std::max(1, K / 256)), 256 / tiles));
+  } else if (M <= 256) {
     // decode-sized batches: workgroup x of a split runs on XCD x % 8, which holds N tiles nt % 8 == j for
     // every M tile.  Split K until the busiest XCD holds one workgroup per CU (32); with long K slices
     // (> 64 k-steps) two per CU.  Fewer splits leave CUs idle, more add partial-sum traffic and a second
@@ -737,9 +776,7 @@ hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M
   if (M <= 0) return hipSuccess;
   if (N % 32 || K % 32) return hipErrorInvalidValue;
   if (M > kRingMaxRows) {  // larger batches: the tile kernel with the same epilogue, one K split
-    const dim3 grid(tile_groups(M, N), 1);
-    launch_tile_kernel<true>(s, grid, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, kslice_for(K, 1),
-                             (uint16_t*)h);
+    launch_tile_kernel<true>(s, 1, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, (uint16_t*)h);
     return hipGetLastError();
   }
   if (use_balanced_swiglu(M, N))

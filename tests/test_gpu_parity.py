@@ -363,6 +363,35 @@ def test_bf16_odd_k_steps_teacher_forced_logits(shape):
     eng.close()
 
 
+# Decode batches of 129..256 rows take the tall tile GEMM (one workgroup holds all activation rows, the weight
+# blocks shared out evenly over the grid); 170 rows leave the last 16-row activation block ragged, and the
+# 512- and 1536-wide K dimensions split into 2 and 6 partials.
+TALL_BF16 = (1, 512, 8, 2, 64, 1536, 2048, 1e6)
+
+
+def test_bf16_tall_decode_batch_teacher_forced_logits():
+    log("bf16 tall decode batch: 10 prompts x G=17 (170 rows) teacher forced")
+    n_prompts, G, P, N = 10, 17, 24, 4
+    S = n_prompts * G
+    cfg = R.model_config(TALL_BF16, R.DTYPE_BF16, P, N, S)
+    eng = R.Engine(cfg)
+    model = OracleModel(shape_of(cfg), mode="bf16")
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=57)
+    u = W.uniforms(S, N, seed=58)
+    ref = rollout(model, prompts, G, N, 1.0, 1.0, u)
+    logits = torch.empty((S, cfg.vocab), dtype=torch.float32, device="cuda:0")
+    R.rollout_prefill(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, logits)
+    eng.synchronize()
+    err = [float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][0])))]
+    for t in range(1, N):
+        R.rollout_decode_step(eng.ctx, to_dev(ref["tokens"][:, t - 1], torch), logits)
+        eng.synchronize()
+        err.append(float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][t]))))
+    log(f"  max abs logit error per step: {[round(e, 5) for e in err]}")
+    assert max(err) <= 3e-2
+    eng.close()
+
+
 def test_device_error_flag_on_bad_token():
     eng, cfg = _tiny_engine()
     prompts = W.prompts(2, 16, cfg.vocab)
