@@ -31,7 +31,11 @@
 // balanced grid instead: one workgroup of two waves per CU, the blocks shared out evenly (BAL below); so
 // does the LM head, with four one-wave workgroups per CU.
 //
-// k_gemm_tile (prefill and other batches above 64 rows): a workgroup of four
+// k_gemm_wlds (decode batches of 129..256 rows): one workgroup holds all activation rows, so each weight
+// byte enters one CU; the weights of a k-step are staged in LDS for the four waves and each wave reads its
+// own activation rows straight from L2 (details at the kernel).
+//
+// k_gemm_tile (prefill, and batches of 65..128 or more than 256 rows): a workgroup of four
 // waves owns 256 weight rows x 128 activation rows; each wave owns its own 64
 // weight rows against all 128 activation rows (4 x 8 MFMA tiles, 128
 // accumulator registers, two waves per SIMD).  The weights never touch LDS:
@@ -72,22 +76,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // Tile kernel: 4 waves; a workgroup owns NB 16-row weight blocks per wave against MBW 16-row activation
-// blocks.  Prefill: NB = 4, MBW = 8 (256 weight rows x 128 activation rows, each wave 64 x 128).  Tall
-// decode batches (129..256 rows): NB = 2, MBW = 16 (128 weight rows x all 256 activation rows), so every
-// weight byte is streamed into one CU only, not once per 128-row activation tile.
+// blocks (NB = 4, MBW = 8: 256 weight rows x 128 activation rows, each wave 64 x 128).
 constexpr int kTileWaves = 4;
-constexpr int kTileNB = 4, kTileMB = 8;  // prefill shape
-constexpr int kTallNB = 2, kTallMB = 16; // tall decode shape
+constexpr int kTileNB = 4, kTileMB = 8;
 
 // SWI: gate/up with SwiGLU applied to the output (one K split): h in the down projection's operand layout
 // XD: activation register stages (each k-step's X fragments are loaded XD steps before they are staged
 // into LDS); OCC: waves per SIMD the registers are sized for.  Batches above 256 rows (prefill, MFMA-bound)
 // take XD = 3 at two waves per SIMD; decode-sized batches, one wave per SIMD anyway, take XD = 6.
-// BAL (one activation tile): the grid's workgroups share the weight blocks out evenly, floor(nbt / grid) or
-// one more each (at most NB * 4); wave w takes the workgroup's blocks NB w .. NB w + NB - 1, and a wave
-// with fewer (or none) loads the workgroup's last block again for them and stores nothing for them.
-// Otherwise workgroups run in XCD-aware order: the M tiles of one N tile share one XCD and its L2.
-template <int NB, int MBW, bool SWI, int XD, int OCC, bool BAL>
+// Workgroups run in XCD-aware order: the M tiles of one N tile share one XCD and its L2.
+template <int NB, int MBW, bool SWI, int XD, int OCC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W, float* __restrict__ out,
                  int M, int N, int K, int kslice, uint16_t* __restrict__ h) {
@@ -96,22 +94,14 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nbt = N >> 4, kbt = K >> 5, Mb = (M + 15) >> 4;
-  int wb0, wbc, mb0;  // the workgroup's first weight block, its block count and its first activation block
-  if constexpr (BAL) {
-    wb0 = (int)((long long)blockIdx.x * nbt / gridDim.x);
-    wbc = (int)((long long)(blockIdx.x + 1) * nbt / gridDim.x) - wb0;
-    mb0 = 0;
-  } else {
-    const int Mt = (Mb + MBW - 1) / MBW, Nt = (nbt + NB * kTileWaves - 1) / (NB * kTileWaves);
-    // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD and its L2
-    const int b = blockIdx.x;
-    const int grp = b / (8 * Mt), rem = b % (8 * Mt);
-    const int nt = grp * 8 + rem % 8, mt = rem / 8;
-    if (nt >= Nt) return;
-    wb0 = nt * NB * kTileWaves;
-    wbc = min(NB * kTileWaves, nbt - wb0);
-    mb0 = mt * MBW;
-  }
+  const int Mt = (Mb + MBW - 1) / MBW, Nt = (nbt + NB * kTileWaves - 1) / (NB * kTileWaves);
+  // XCD-aware order (workgroup b runs on XCD b % 8): the M tiles of N tile nt share one XCD and its L2
+  const int b = blockIdx.x;
+  const int grp = b / (8 * Mt), rem = b % (8 * Mt);
+  const int nt = grp * 8 + rem % 8, mt = rem / 8;
+  if (nt >= Nt) return;
+  // the workgroup's first weight block and its block count, its first activation block
+  const int wb0 = nt * NB * kTileWaves, wbc = min(NB * kTileWaves, nbt - wb0), mb0 = mt * MBW;
   const int lb0 = wave * NB;  // the wave's first block within the workgroup's
   const int kb0 = (int)blockIdx.y * (kslice >> 5);
   const int nk = min(kbt, kb0 + (kslice >> 5)) - kb0;
@@ -199,6 +189,127 @@ void k_gemm_tile(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W
 #pragma unroll
     for (int i = 0; i < MBW; ++i) {
       const int m = (mb0 + i) * 16 + (lane & 15);
+      if (m >= M) continue;
+      if constexpr (SWI) {
+        // rows n, n+1 are (gate, up) of output f = n/2; rows n+2, n+3 of output f + 1
+        const float g0 = acc[j][i][0], u0 = acc[j][i][1], g1 = acc[j][i][2], u1 = acc[j][i][3];
+        const float h0 = g0 / (1.0f + expf(-g0)) * u0, h1 = g1 / (1.0f + expf(-g1)) * u1;
+        *reinterpret_cast<uint32_t*>(h + xoff(h, m, n >> 1, N >> 1, Mb)) = pack_bf16x2(h0, h1);
+      } else {
+        *reinterpret_cast<float4*>(o + (size_t)m * N + n) = make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
+      }
+    }
+  }
+}
+
+// Tall decode batches (129..256 rows), weights staged in LDS: a workgroup of four waves owns up to
+// kWldsBlocks weight blocks (128 rows; the grid shares the blocks out evenly, floor(nbt / grid) or one more
+// each) and all 16 activation blocks; wave w owns activation blocks 4w .. 4w + 3 against every weight block
+// of the workgroup (8 x 4 MFMA tiles).  A k-step's weight fragments (8 KB) are streamed from HBM once per
+// workgroup -- each wave stages two of them, global -> registers (three steps ahead) -> LDS (double
+// buffered) -- and read from LDS by all four waves, while each wave loads its own activation fragments
+// from L2 straight into registers, XD steps ahead.  Per k-step and CU: 40 KB of LDS traffic for 128 MFMAs
+// (staging the 16 KB activation tile instead would take 80 KB), and every weight byte enters one CU.
+// One LDS barrier per k-step; loads are unconditional (indices clamped, surplus steps not computed).
+constexpr int kWldsBlocks = 8;
+template <bool SWI, int XD, int WD>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_gemm_wlds(const bf16x8_t* __restrict__ XF, const bf16x8_t* __restrict__ W, float* __restrict__ out, int M,
+                 int N, int K, int kslice, uint16_t* __restrict__ h) {
+  constexpr int NBG = kWldsBlocks;           // weight blocks per workgroup
+  constexpr int MBV = 4;                     // activation blocks per wave
+  constexpr int WPW = NBG / kTileWaves;      // weight fragments each wave stages per k-step
+  __shared__ bf16x8_t wl[2][NBG][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nbt = N >> 4, kbt = K >> 5, Mb = (M + 15) >> 4;
+  const int wb0 = (int)((long long)blockIdx.x * nbt / gridDim.x);
+  const int wbc = (int)((long long)(blockIdx.x + 1) * nbt / gridDim.x) - wb0;
+  const int kb0 = (int)blockIdx.y * (kslice >> 5);
+  const int nk = min(kbt, kb0 + (kslice >> 5)) - kb0;
+  floatx4_t acc[NBG][MBV];
+#pragma unroll
+  for (int j = 0; j < NBG; ++j)
+#pragma unroll
+    for (int i = 0; i < MBV; ++i) acc[j][i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  if (nk > 0) {
+    const bf16x8_t* wp[WPW];
+    int wsd[WPW];  // k-step stride of each staged block's fragments
+#pragma unroll
+    for (int j = 0; j < WPW; ++j) {
+      const int nb = wb0 + min(WPW * wave + j, wbc - 1);
+      wp[j] = W + wfrag(nb, kb0, nbt, kbt) * 64 + lane;
+      wsd[j] = wgroup_blocks(nb, nbt) * 64;
+    }
+    const bf16x8_t* xp[MBV];
+#pragma unroll
+    for (int i = 0; i < MBV; ++i) xp[i] = XF + ((size_t)kb0 * Mb + min(MBV * wave + i, Mb - 1)) * 64 + lane;
+    const size_t xstride = (size_t)Mb * 64;
+    static_assert(6 % XD == 0 && 6 % WD == 0 && WD >= 3, "the k-step loop is unrolled by 6");
+    bf16x8_t wg[WD][WPW], xr[XD][MBV], wf[2][NBG];
+    auto load_w = [&](int slot, int st) {
+      const size_t kk = (size_t)min(st, nk - 1);
+#pragma unroll
+      for (int j = 0; j < WPW; ++j) wg[slot][j] = __builtin_nontemporal_load(wp[j] + kk * wsd[j]);
+    };
+    auto store_w = [&](int buf, int slot) {
+#pragma unroll
+      for (int j = 0; j < WPW; ++j) wl[buf][WPW * wave + j][lane] = wg[slot][j];
+    };
+    auto read_w = [&](int reg, int buf) {
+#pragma unroll
+      for (int j = 0; j < NBG; ++j) wf[reg][j] = wl[buf][j][lane];
+    };
+    auto load_x = [&](int slot, int st) {
+      const size_t kk = (size_t)min(st, nk - 1);
+#pragma unroll
+      for (int i = 0; i < MBV; ++i) xr[slot][i] = xp[i][kk * xstride];
+    };
+    // W(k) passes through global register slot k % WD, LDS buffer k % 2 and fragment registers wf[k % 2].
+    // k-step st multiplies wf[st % 2] (read from LDS during step st - 1) with activation slot st % XD, and
+    // meanwhile reads W(st + 1) out of LDS, writes W(st + 2) into the LDS buffer W(st) came from (every wave
+    // finished reading it before the barrier that ended step st - 1), loads W(st + 2 + WD) into the freed
+    // register slot and X(st + XD) into its slot.  WD - 2 steps of weights stay in flight; one barrier per
+    // step.
+#pragma unroll
+    for (int d = 0; d < WD; ++d) load_w(d, d);
+#pragma unroll
+    for (int d = 0; d < XD; ++d) load_x(d, d);
+    store_w(0, 0);
+    store_w(1, 1);
+    load_w(0, WD);
+    load_w(1, WD + 1);
+    lds_barrier();
+    read_w(0, 0);
+    lds_barrier();  // every wave holds W(0) before step 0 overwrites LDS buffer 0
+    for (int s0 = 0; s0 < nk; s0 += 6) {
+#pragma unroll
+      for (int u = 0; u < 6; ++u) {
+        const int st = s0 + u;
+        read_w((u + 1) & 1, (u + 1) & 1);
+        store_w(u & 1, (u + 2) % WD);
+        load_w((u + 2) % WD, st + 2 + WD);
+        if (st < nk) {
+#pragma unroll
+          for (int j = 0; j < NBG; ++j)
+#pragma unroll
+            for (int i = 0; i < MBV; ++i)
+              acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[u & 1][j], xr[u % XD][i], acc[j][i], 0, 0, 0);
+        }
+        load_x(u % XD, st + XD);
+        lds_barrier();
+      }
+    }
+  }
+  // D layout of the 16x16 MFMA: lane holds rows 4*(lane/16)+r (weight rows n) of column lane%16 (row m of X)
+  float* o = out + (size_t)blockIdx.y * M * N;
+#pragma unroll
+  for (int j = 0; j < NBG; ++j) {
+    if (j >= wbc) continue;
+    const int n = (wb0 + j) * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int i = 0; i < MBV; ++i) {
+      const int m = (MBV * wave + i) * 16 + (lane & 15);
       if (m >= M) continue;
       if constexpr (SWI) {
         // rows n, n+1 are (gate, up) of output f = n/2; rows n+2, n+3 of output f + 1
@@ -550,10 +661,10 @@ int tile_m_tiles(int M) { return ((M + 15) / 16 + kTileMB - 1) / kTileMB; }
 int tile_n_tiles(int N) { return (N / 16 + kTileNB * kTileWaves - 1) / (kTileNB * kTileWaves); }
 int tile_groups(int M, int N) { return (tile_n_tiles(N) + 7) / 8 * 8 * tile_m_tiles(M); }
 
-// Tall decode batches (129..256 rows, one activation tile): balanced grid of workgroups with at most
-// kTallNB * 4 weight blocks each, about one per CU per K split.
+// Tall decode batches (129..256 rows, one activation tile) take k_gemm_wlds on a balanced grid of
+// workgroups with at most kWldsBlocks weight blocks each, about one per CU per K split.
 constexpr int kTallMinRows = 129, kTallMaxRows = 256;
-constexpr int kTallWgBlocks = kTallNB * kTileWaves;
+constexpr int kTallWgBlocks = kWldsBlocks;
 bool tall_batch(int M) { return M >= kTallMinRows && M <= kTallMaxRows; }
 int tall_groups(int N, int splits) {
   const int nbt = N / 16;
@@ -572,13 +683,13 @@ void launch_tile_kernel(hipStream_t s, int splits, const bf16x8_t* x, const bf16
   const dim3 block(64 * kTileWaves);
   if (tall_batch(M)) {
     const dim3 grid(tall_groups(N, splits), splits);
-    hipLaunchKernelGGL((k_gemm_tile<kTallNB, kTallMB, SWI, 6, 1, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+    hipLaunchKernelGGL((k_gemm_wlds<SWI, 3, 3>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
   } else if (M <= kTileDecodeRows) {
     const dim3 grid(tile_groups(M, N), splits);
-    hipLaunchKernelGGL((k_gemm_tile<kTileNB, kTileMB, SWI, 6, 1, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+    hipLaunchKernelGGL((k_gemm_tile<kTileNB, kTileMB, SWI, 6, 1>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
   } else {
     const dim3 grid(tile_groups(M, N), splits);
-    hipLaunchKernelGGL((k_gemm_tile<kTileNB, kTileMB, SWI, 3, 2, false>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
+    hipLaunchKernelGGL((k_gemm_tile<kTileNB, kTileMB, SWI, 3, 2>), grid, block, 0, s, x, w, out, M, N, K, kslice, h);
   }
 }
 
