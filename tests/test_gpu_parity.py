@@ -392,6 +392,37 @@ def test_bf16_tall_decode_batch_teacher_forced_logits():
     eng.close()
 
 
+# The shared-prefix pass at many groups (384 and 640 rows, decode on the tile GEMM) with eight query heads
+# per KV head: 64 groups of 6 (three full 16-column tiles per group and KV head) and 128 groups of 5 (40
+# columns, the last tile half filled).
+WIDE_PREFIX_BF16 = (1, 512, 16, 2, 64, 512, 2048, 1e6)
+
+
+@pytest.mark.parametrize("n_prompts,G", [(64, 6), (128, 5)])
+def test_bf16_shared_prefix_wide_workgroups_teacher_forced(n_prompts, G, monkeypatch):
+    set_attn_knobs(monkeypatch, "2", None)
+    log(f"bf16 shared prefix, {n_prompts} prompts x G={G}, 8 query heads per KV head, teacher forced")
+    P, N = 40, 3
+    S = n_prompts * G
+    cfg = R.model_config(WIDE_PREFIX_BF16, R.DTYPE_BF16, P, N, S)
+    eng = R.Engine(cfg, group_size=G)
+    model = OracleModel(shape_of(cfg), mode="bf16")
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=63)
+    u = W.uniforms(S, N, seed=64)
+    ref = rollout(model, prompts, G, N, 1.0, 1.0, u)
+    logits = torch.empty((S, cfg.vocab), dtype=torch.float32, device="cuda:0")
+    R.rollout_prefill(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, logits)
+    eng.synchronize()
+    err = [float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][0])))]
+    for t in range(1, N):
+        R.rollout_decode_step(eng.ctx, to_dev(ref["tokens"][:, t - 1], torch), logits)
+        eng.synchronize()
+        err.append(float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][t]))))
+    log(f"  max abs logit error per step: {[round(e, 5) for e in err]}")
+    assert max(err) <= 3e-2
+    eng.close()
+
+
 def test_device_error_flag_on_bad_token():
     eng, cfg = _tiny_engine()
     prompts = W.prompts(2, 16, cfg.vocab)
