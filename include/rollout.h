@@ -308,6 +308,26 @@ typedef struct {
 rollout_status rollout_profile_decode_step(rollout_ctx* ctx, const int32_t* d_tokens, float* d_logits,
                                            rollout_step_profile* out);
 
+/* Average duration of the projection GEMMs of one decode step of the current
+ * wave, in the launch mode the rollout uses: the step's projection launches
+ * (per layer QKV, O, gate/up with SwiGLU, down; then the LM head, into
+ * d_logits, fp32 [n_seqs, vocab]) are captured as one HIP graph and replayed
+ * reps times between two HIP events on the context's stream.  Only the
+ * split-K workspace, the SwiGLU output and d_logits are written (the wave's
+ * KV cache, residual stream and positions are untouched).  out: launches per
+ * step, average microseconds per launch, algorithmic bytes (weights once,
+ * activations and outputs once) and flops per launch on average.
+ * Errors: EINVAL (reps < 1, NULL; int4 weights with more than 64 rows in the
+ * wave, whose projections dequantise first), ESTATE (no wave), EDEVICE. */
+typedef struct {
+  int32_t launches;
+  double avg_us;
+  double bytes_per_launch;
+  double flops_per_launch;
+} rollout_projection_profile;
+rollout_status rollout_profile_projections(rollout_ctx* ctx, int32_t reps, float* d_logits,
+                                           rollout_projection_profile* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,7 +26,7 @@ EXPORTED = (
     "rollout_plan", "rollout_init", "rollout_prefill", "rollout_decode_step", "rollout_sample",
     "grpo_advantages", "rollout_generate", "rollout_sync", "rollout_destroy", "rollout_last_error",
     "rollout_export_weight", "rollout_profile_decode_step", "rollout_generate_eos", "rollout_length_rewards",
-    "rollout_sample_noalloc",
+    "rollout_sample_noalloc", "rollout_profile_projections",
 )
 NOALLOC_SCRATCH_BYTES = 64 << 20  # ROLLOUT_SAMPLE_NOALLOC_SCRATCH_BYTES
 # include/occupancy.h: power metrics and threshold policy of the occupancy controller (host code)
@@ -70,6 +70,13 @@ class OccReading(ctypes.Structure):
     ]
 
 
+class ProjectionProfile(ctypes.Structure):
+    _fields_ = [
+        ("launches", ctypes.c_int32), ("avg_us", ctypes.c_double), ("bytes_per_launch", ctypes.c_double),
+        ("flops_per_launch", ctypes.c_double),
+    ]
+
+
 class StepProfile(ctypes.Structure):
     _fields_ = [
         ("ms", ctypes.c_double * 3), ("launches", ctypes.c_int32 * 3),
@@ -104,6 +111,7 @@ def _load():
                                   ctypes.POINTER(i32)], i32),
         "rollout_length_rewards": ([vp, i32, i32, vp, vp, vp], i32),
         "rollout_sample_noalloc": ([vp, i32, i32, f32, f32, vp, vp, vp], i32),
+        "rollout_profile_projections": ([vp, i32, vp, ctypes.POINTER(ProjectionProfile)], i32),
         "occ_rolling_mean": ([vp, ctypes.c_int64, f64, f64, vp], i32),
         "occ_violation": ([vp, ctypes.c_int64, f64, f64, ctypes.POINTER(f64), ctypes.POINTER(f64)], i32),
         "occ_normalize_budget": ([f64, f64, f64], f64),
@@ -214,6 +222,12 @@ def rollout_last_error(ctx=None) -> str:
 
 def rollout_export_weight(ctx, tensor_id: int, out):
     _check(lib.rollout_export_weight(ctx, tensor_id, _ptr(out)), ctx)
+
+
+def rollout_profile_projections(ctx, reps: int, logits) -> ProjectionProfile:
+    out = ProjectionProfile()
+    _check(lib.rollout_profile_projections(ctx, reps, _ptr(logits), ctypes.byref(out)), ctx)
+    return out
 
 
 def rollout_profile_decode_step(ctx, tokens, logits) -> StepProfile:

@@ -1212,4 +1212,90 @@ rollout_status rollout_profile_decode_step(rollout_ctx* ctx, const int32_t* d_to
   return ROLLOUT_OK;
 }
 
+rollout_status rollout_profile_projections(rollout_ctx* ctx, int32_t reps, float* d_logits,
+                                           rollout_projection_profile* out) {
+  if (!ctx) return fail(nullptr, ROLLOUT_EINVAL, "ctx is NULL");
+  if (!out || !d_logits || reps < 1) return fail(ctx, ROLLOUT_EINVAL, "out and logits must be non-NULL, reps >= 1");
+  if (!ctx->wave) return fail(ctx, ROLLOUT_ESTATE, "no wave (prefill first)");
+  const Dims& D = ctx->D;
+  const Layout& Lo = ctx->Lo;
+  const int M = ctx->S;
+  if (D.wq4 && M > kSwigluMaxRows)
+    return fail(ctx, ROLLOUT_EINVAL, "int4 batches over " + std::to_string(kSwigluMaxRows) +
+                                         " rows dequantise before their GEMMs: not one launch per projection");
+  const bool fused = D.dtype == ROLLOUT_DTYPE_BF16;
+  void* a = ctx->at(Lo.a);
+  void* o = ctx->at(Lo.o);
+  void* h = ctx->at(Lo.h);
+  float* part = ctx->at<float>(Lo.part);
+  const double eb = (double)elem_bytes(D.dtype);
+  auto wbytes = [&](int N, int K) {
+    return D.wq4 ? (double)(q4_code_bytes(N, K) + q4_sz_bytes(N, K)) : (double)N * K * eb;
+  };
+  double bytes = 0.0, flops = 0.0;
+  int launches = 0;
+  // the projection launches of forward_layers and enqueue_decode at M = S rows, in step order
+  auto enqueue = [&]() -> rollout_status {
+    int s = 0;
+    rollout_status r;
+    for (int l = 0; l < D.L; ++l) {
+      const Layer& y = Lo.layers[l];
+      if ((r = proj(ctx, a, ctx->at(y.wqkv), part, M, D.nqkv, D.d, &s))) return r;
+      if ((r = proj(ctx, o, ctx->at(y.wo), part, M, D.d, D.qd, &s))) return r;
+      if (fused) {
+        if ((r = gemm_swiglu(ctx, a, ctx->at(y.wgu), M, 2 * D.ff, D.d, h))) return r;
+      } else {
+        if ((r = proj(ctx, a, ctx->at(y.wgu), part, M, 2 * D.ff, D.d, &s))) return r;
+      }
+      if ((r = proj(ctx, h, ctx->at(y.wdown), part, M, D.d, D.ff, &s))) return r;
+    }
+    return gemm(ctx, a, ctx->at(Lo.lm_head), d_logits, M, D.V, D.d, 1, &s);
+  };
+  for (int l = 0; l < D.L; ++l) {
+    bytes += wbytes(D.nqkv, D.d) + (double)M * D.d * eb + (double)M * D.nqkv * 4;
+    bytes += wbytes(D.d, D.qd) + (double)M * D.qd * eb + (double)M * D.d * 4;
+    bytes += wbytes(2 * D.ff, D.d) + (double)M * D.d * eb + (fused ? (double)M * D.ff * eb : (double)M * 2 * D.ff * 4);
+    bytes += wbytes(D.d, D.ff) + (double)M * D.ff * eb + (double)M * D.d * 4;
+    flops += 2.0 * M * ((double)D.nqkv * D.d + (double)D.d * D.qd + 2.0 * D.ff * D.d + (double)D.d * D.ff);
+    launches += 4;
+  }
+  bytes += (double)D.V * D.d * eb + (double)M * D.d * eb + (double)M * D.V * 4;
+  flops += 2.0 * M * (double)D.V * D.d;
+  launches += 1;
+  Range range("rollout_profile_projections");
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  HIP_TRY(ctx, hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal), "begin capture");
+  rollout_status r = enqueue();
+  hipError_t ce = hipStreamEndCapture(ctx->stream, &graph);
+  if (r) {
+    if (graph) hipGraphDestroy(graph);
+    return r;
+  }
+  if (ce != hipSuccess) return hip_fail(ctx, ce, "end capture");
+  hipError_t e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  if (e != hipSuccess) return hip_fail(ctx, e, "graph instantiate");
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) e = hipGraphLaunch(exec, ctx->stream);  // warm-up replay
+  if (e == hipSuccess) e = hipEventRecord(e0, ctx->stream);
+  for (int i = 0; i < reps && e == hipSuccess; ++i) e = hipGraphLaunch(exec, ctx->stream);
+  if (e == hipSuccess) e = hipEventRecord(e1, ctx->stream);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  hipStreamSynchronize(ctx->stream);
+  hipGraphExecDestroy(exec);
+  if (e0) hipEventDestroy(e0);
+  if (e1) hipEventDestroy(e1);
+  if (e != hipSuccess) return hip_fail(ctx, e, "projection replay");
+  out->launches = launches;
+  out->avg_us = (double)ms * 1e3 / ((double)reps * launches);
+  out->bytes_per_launch = bytes / launches;
+  out->flops_per_launch = flops / launches;
+  return ROLLOUT_OK;
+}
+
 }  // extern "C"

@@ -125,7 +125,8 @@ def test_validation_before_device_work():
         R.grpo_advantages(0x1000, 0, 8, 0.0, 1, 0x2000)
     assert e.value.code == R.EINVAL
     for fn, args in ((R.rollout_prefill, (0x1000, 1, 4, 1, 0x2000)), (R.rollout_decode_step, (0x1000, 0x2000)),
-                     (R.rollout_sample, (0x1000, 1, 1.0, 1.0, 0x2000, 0x3000)), (R.rollout_sync, ())):
+                     (R.rollout_sample, (0x1000, 1, 1.0, 1.0, 0x2000, 0x3000)), (R.rollout_sync, ()),
+                     (R.rollout_profile_projections, (1, 0x2000))):
         with pytest.raises(R.RolloutError) as e:
             fn(None, *args)
         assert e.value.code == R.EINVAL
