@@ -17,8 +17,9 @@
 // chosen from mass histograms.  Ties at tau are kept lowest id first.
 //
 // Two implementations of the same integers.  Chunked (fewer rows): every
-// pass over a row's V values runs as rows x chunks workgroups (chunk
-// max; exp stored once with the chunk mass and first-digit histogram; one
+// pass over a row's V values runs as rows x chunks workgroups, a chunk being
+// a whole number of 4096-id batches that a workgroup loads in one round trip
+// (chunk max; exp stored once with the chunk mass and first-digit histogram; one
 // histogram pass per remaining digit; per-chunk kept mass and tie count);
 // between passes a small kernel per row picks the digit with a parallel
 // suffix scan over the 256 bins.  The final kernel per row scans the chunk
@@ -38,6 +39,8 @@ namespace {
 constexpr int CB = 256;  // threads of the per-chunk kernels
 constexpr int CW = CB / 64;
 constexpr int kMaxChunks = 64;  // chunks per row (sample_chunks caps nc here)
+constexpr int kPer = 16;        // ids per thread in one batch of a chunk kernel
+constexpr int kBatch = CB * kPer;  // ids per batch; a chunk is a whole number of batches
 constexpr int RB = 1024;  // threads of the per-row draw kernel
 constexpr int RW = RB / 64;
 typedef unsigned long long u64;
@@ -77,6 +80,14 @@ __device__ __forceinline__ float row_max(const float* cm, int nc) {
   return m;
 }
 
+// One batch of a chunk: thread t takes ids b + j * CB + t (j < kPer), all kPer loads in flight before
+// the first is used.  Ids at or past hi read id hi - 1 (hi > b) and are masked where the values are used,
+// unconditionally (a select, not a branch), so the compiler keeps the loads together.
+__device__ __forceinline__ void load_batch(const float* __restrict__ row, int b, int hi, float* v) {
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) v[j] = row[min(b + j * CB + (int)threadIdx.x, hi - 1)];
+}
+
 __device__ __forceinline__ u64 wave_sum_u64(u64 v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -108,7 +119,15 @@ __global__ __launch_bounds__(CB) void k_chunk_argmax(const float* __restrict__ l
   const int lo = c * chunk, hi = min(V, lo + chunk);
   float best = -INFINITY;
   int bi = INT_MAX;
-  for (int i = lo + tid; i < hi; i += CB) better(best, bi, z[i], i);
+  for (int b = lo; b < hi; b += kBatch) {
+    float v[kPer];
+    load_batch(z, b, hi, v);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = b + j * CB + tid;
+      better(best, bi, i < hi ? v[j] : -INFINITY, i < hi ? i : INT_MAX);
+    }
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) better(best, bi, __shfl_xor(best, o, 64), __shfl_xor(bi, o, 64));
   if (lane == 0) { rv[w] = best; ri[w] = bi; }
@@ -143,7 +162,12 @@ __global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logi
   const float* z = logits + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
   float mx = -INFINITY;
-  for (int i = lo + tid; i < hi; i += CB) mx = fmaxf(mx, z[i] / T);
+  for (int b = lo; b < hi; b += kBatch) {
+    float v[kPer];
+    load_batch(z, b, hi, v);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) mx = fmaxf(mx, b + j * CB + tid < hi ? v[j] / T : -INFINITY);
+  }
   mx = wave_max(mx);
   if ((tid & 63) == 0) red[tid >> 6] = mx;
   __syncthreads();
@@ -169,12 +193,20 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
     __syncthreads();
   }
   u64 mass = 0;
-  for (int i = lo + tid; i < hi; i += CB) {
-    const float e = expf(z[i] / T - m);
-    e_row[i] = e;
-    const u64 f = fx40(e);
-    mass += f;
-    if (filter) atomicAdd(&hist[w][__float_as_uint(e) >> 24], f);
+  for (int b = lo; b < hi; b += kBatch) {
+    float v[kPer];
+    load_batch(z, b, hi, v);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = b + j * CB + tid;
+      const float e = expf(v[j] / T - m);
+      const u64 f = i < hi ? fx40(e) : 0ull;
+      mass += f;
+      if (i < hi) {
+        e_row[i] = e;
+        if (filter) atomicAdd(&hist[w][__float_as_uint(e) >> 24], f);
+      }
+    }
   }
   mass = wave_sum_u64(mass);
   if ((tid & 63) == 0) red[w] = mass;
@@ -262,10 +294,14 @@ __global__ __launch_bounds__(CB) void k_chunk_hist(const float* __restrict__ esc
   const int lo = c * chunk, hi = min(V, lo + chunk);
   for (int i = tid; i < CW * 256; i += CB) (&hist[0][0])[i] = 0;
   __syncthreads();
-  for (int i = lo + tid; i < hi; i += CB) {
-    const float e = e_row[i];
-    const unsigned b = __float_as_uint(e);
-    if ((b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(e));
+  for (int b0 = lo; b0 < hi; b0 += kBatch) {
+    float v[kPer];
+    load_batch(e_row, b0, hi, v);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const unsigned b = __float_as_uint(v[j]);
+      if (b0 + j * CB + tid < hi && (b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(v[j]));
+    }
   }
   __syncthreads();
   u64 t = 0;
@@ -283,11 +319,17 @@ __global__ __launch_bounds__(CB) void k_chunk_kept(const float* __restrict__ esc
   const float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
   u64 gt = 0, ties = 0;
-  for (int i = lo + tid; i < hi; i += CB) {
-    const float e = e_row[i];
-    const unsigned b = __float_as_uint(e);
-    if (!filter || b > tau) gt += fx40(e);
-    else if (b == tau) ties += 1;
+  for (int b0 = lo; b0 < hi; b0 += kBatch) {
+    float v[kPer];
+    load_batch(e_row, b0, hi, v);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const bool ok = b0 + j * CB + tid < hi;
+      const unsigned b = __float_as_uint(v[j]);
+      const u64 f = fx40(v[j]);
+      gt += ok && (!filter || b > tau) ? f : 0ull;
+      ties += ok && filter && b == tau ? 1ull : 0ull;
+    }
   }
   gt = wave_sum_u64(gt);
   ties = wave_sum_u64(ties);
@@ -359,10 +401,19 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
   const int seg = ((hi_c - lo_c + RW - 1) / RW + 63) / 64 * 64;
   const int lo = min(hi_c, lo_c + w * seg), hi = min(hi_c, lo + seg);
   u64 gt = 0, ties = 0;
-  for (int i = lo + lane; i < hi; i += 64) {
-    const unsigned b = __float_as_uint(e_row[i]);
-    if (!filter || b > tau) gt += fx40(e_row[i]);
-    else if (b == tau) ties += 1;
+  // four 64-id steps of the segment per round trip (clamped to the segment's last id, masked at use)
+  for (int b0 = lo; b0 < hi; b0 += 4 * 64) {
+    float v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = e_row[min(b0 + j * 64 + lane, hi - 1)];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = b0 + j * 64 + lane < hi;
+      const unsigned b = __float_as_uint(v[j]);
+      const u64 f = fx40(v[j]);
+      gt += ok && (!filter || b > tau) ? f : 0ull;
+      ties += ok && filter && b == tau ? 1ull : 0ull;
+    }
   }
   gt = wave_sum_u64(gt);
   ties = wave_sum_u64(ties);
@@ -381,24 +432,34 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
   const u64 my_mass = gt + my_kept_ties * ftau;
   if (my_mass > 0 && excl <= thresh && thresh < excl + my_mass) {
     u64 carry = excl, tie_carry = 0;
-    for (int base = lo; base < hi; base += 64) {
-      const int i = base + lane;
-      const float e = i < hi ? e_row[i] : 0.f;
-      const unsigned b = __float_as_uint(e);
-      bool keep = i < hi && (!filter || b > tau);
-      if (filter) {
-        const bool is_tie = i < hi && b == tau;
-        const u64 tie_incl = wave_incl_scan(is_tie ? 1ull : 0ull, lane);
-        if (is_tie && tie_carry + tie_incl - 1 < my_kept_ties) keep = true;
-        tie_carry += __shfl(tie_incl, 63, 64);
+    bool found = false;
+    for (int b0 = lo; b0 < hi && !found; b0 += 4 * 64) {
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = e_row[min(b0 + j * 64 + lane, hi - 1)];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int base = b0 + j * 64;
+        if (found || base >= hi) break;  // wave-uniform
+        const int i = base + lane;
+        const float e = i < hi ? v[j] : 0.f;
+        const unsigned b = __float_as_uint(e);
+        bool keep = i < hi && (!filter || b > tau);
+        if (filter) {
+          const bool is_tie = i < hi && b == tau;
+          const u64 tie_incl = wave_incl_scan(is_tie ? 1ull : 0ull, lane);
+          if (is_tie && tie_carry + tie_incl - 1 < my_kept_ties) keep = true;
+          tie_carry += __shfl(tie_incl, 63, 64);
+        }
+        const u64 cum = carry + wave_incl_scan(keep ? fx40(e) : 0ull, lane);
+        const unsigned long long hit = __ballot(keep && cum > thresh);
+        if (hit) {
+          if (lane == __ffsll((long long)hit) - 1) s_tok = i;
+          found = true;
+        } else {
+          carry = __shfl(cum, 63, 64);
+        }
       }
-      const u64 cum = carry + wave_incl_scan(keep ? fx40(e) : 0ull, lane);
-      const unsigned long long hit = __ballot(keep && cum > thresh);
-      if (hit) {
-        if (lane == __ffsll((long long)hit) - 1) s_tok = i;
-        break;
-      }
-      carry = __shfl(cum, 63, 64);
     }
   }
   __syncthreads();
@@ -676,9 +737,16 @@ bool use_row_sampler(int S, int V) {
 
 }  // namespace
 
+// Ids per chunk: the fewest whole batches that keep a row within kMaxChunks chunks.
+int sample_chunk_ids(int V) {
+  const long long per = ((long long)V + kMaxChunks - 1) / kMaxChunks;
+  const long long b = (per + kBatch - 1) / kBatch;
+  return (int)((b < 1 ? 1 : b) * kBatch);
+}
+
 int sample_chunks(int V) {
-  const int c = (V + 4095) / 4096;
-  return c < 1 ? 1 : (c > 64 ? 64 : c);
+  const int c = (int)(((long long)V + sample_chunk_ids(V) - 1) / sample_chunk_ids(V));
+  return c < 1 ? 1 : c;
 }
 
 size_t sample_scratch_bytes(int S, int V) {
@@ -701,7 +769,7 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
                          void* scratch) {
   if (S <= 0) return hipSuccess;
   const int nc = sample_chunks(V);
-  const int chunk = (V + nc - 1) / nc;
+  const int chunk = sample_chunk_ids(V);
   char* p = (char*)scratch;
   auto take = [&](size_t bytes) {
     char* q = p;

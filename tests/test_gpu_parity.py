@@ -85,7 +85,9 @@ def test_weights_bit_exact(dtype, shape):
 # ---------------------------------------------------------------------------
 # sampler on identical logits
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("V", [1024, 2048, 152064])
+# vocabularies: one chunk; 152064 (38 chunks of 4096 ids, the last of 512); 300000 (above 64 x 4096: chunks
+# of two 4096-id batches).  Widths that are not a multiple of 16 go through rollout_sample_noalloc.
+@pytest.mark.parametrize("V", [1024, 2048, 152064, 300000])
 @pytest.mark.parametrize("temperature,top_p", [(0.0, 1.0), (1.0, 1.0), (0.9, 0.95), (0.7, 0.5), (1.0, 1e-6)])
 def test_sampler_matches_oracle(V, temperature, top_p):
     log(f"sampler V={V} T={temperature} top_p={top_p}")
@@ -121,7 +123,7 @@ def test_sampler_matches_oracle(V, temperature, top_p):
     eng.close()
 
 
-@pytest.mark.parametrize("V", [1024, 2064, 152064])
+@pytest.mark.parametrize("V", [1024, 2064, 152064, 262144])
 @pytest.mark.parametrize("temperature,top_p", [(1.0, 1.0), (0.9, 0.95), (0.7, 0.5), (1.0, 1e-6)])
 def test_sampler_row_kernel_equals_chunked_kernels(V, temperature, top_p, monkeypatch):
     """The one-workgroup-per-row sampler and the chunked kernels draw the same token from the same logits

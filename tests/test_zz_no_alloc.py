@@ -1,7 +1,8 @@
 """rollout_sample_noalloc, the allocation-free draw: the same tokens as rollout_sample, the entry point it is a
 variant of, on the same logits and uniforms -- bit for bit (both decide in exact integers) -- on two calls in
-a row, the second with fewer rows; rows beyond one batch of the fixed scratch; and argument validation that
-happens before any device work."""
+a row, the second with fewer rows; rows beyond one batch of the fixed scratch; vocabularies that no context
+can have (not a multiple of 16), against the oracle; and argument validation that happens before any device
+work."""
 import numpy as np
 import pytest
 
@@ -52,6 +53,38 @@ def test_noalloc_draw_in_several_batches_of_the_fixed_scratch():
     print(f"noalloc sampler V={V}: {S} rows in batches", flush=True)
     got, want = _draw_both(V, S, 0.9, 0.95, 11)
     assert np.array_equal(got, want), np.nonzero(got != want)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("V", [3, 4099])
+@pytest.mark.parametrize("T,top_p", [(0.0, 1.0), (1.0, 1.0), (0.9, 0.95), (0.7, 0.5)])
+def test_noalloc_draw_matches_the_oracle_at_vocabularies_no_context_has(V, T, top_p):
+    # the row width is an argument here, so any vocabulary of at least 2 ids reaches the chunked kernels:
+    # 4099 = one 4096-id chunk and one of 3 ids (rows not 16-byte aligned), 3 = one short chunk
+    from oracle import sample_row
+
+    S = 48
+    rng = np.random.default_rng(V + 5)
+    z = (rng.standard_normal((S, V)) * 2.0).astype(np.float32)
+    z[:4] = np.round(z[:4], 1)  # ties in value
+    u = W.uniforms(S, 1, seed=V)[:, 0]
+    print(f"noalloc sampler V={V} T={T} top_p={top_p}: {S} rows against the oracle", flush=True)
+    dev = "cuda:0"
+    got = torch.full((S,), -1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream(device=dev)
+    R.rollout_sample_noalloc(torch.from_numpy(z).to(dev), S, V, T, top_p, torch.from_numpy(u).to(dev), got,
+                             stream.cuda_stream)
+    stream.synchronize()
+    got = got.cpu().numpy()
+    assert np.all((got >= 0) & (got < V))
+    checked = 0
+    for s in range(S):
+        tok, margin = sample_row(z[s], T, top_p, float(u[s]))
+        if margin < 1e-6:  # a draw within rounding of flipping (see the sampler parity test)
+            continue
+        assert got[s] == tok, f"row {s}: gpu {got[s]} oracle {tok} margin {margin}"
+        checked += 1
+    assert checked >= S - 8
 
 
 def test_noalloc_validates_before_any_device_work():
