@@ -17,11 +17,12 @@ import numpy as np
 
 COPY_BYTES = 1 << 30
 
-# shape name, prompts, prompt length, G, sequences in flight, new tokens
+# shape name, prompts, prompt length, G, sequences in flight, new tokens, int4 layer projections
 WORKLOADS = {
-    "7b": ("7b", 8, 256, 8, 64, 512),
-    "14b": ("14b", 16, 512, 16, 256, 1024),
-    "72b": ("72b", 8, 512, 8, 64, 512),
+    "7b": ("7b", 8, 256, 8, 64, 512, False),
+    "14b": ("14b", 16, 512, 16, 256, 1024, False),
+    "72b": ("72b", 8, 512, 8, 64, 512, False),
+    "72b-int4": ("72b", 8, 512, 8, 64, 512, True),
 }
 
 
@@ -36,9 +37,9 @@ def main():
     import paper_2608_11226_amd as R
     import workload as W
 
-    shape, n_prompts, P, G, S, N = WORKLOADS[args.workload]
+    shape, n_prompts, P, G, S, N, q4 = WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
-    eng = R.Engine(R.model_config(shape, R.DTYPE_BF16, P, N, S), group_size=G)
+    eng = R.Engine(R.model_config(shape, R.DTYPE_INT4 if q4 else R.DTYPE_BF16, P, N, S), group_size=G)
     V = R.SHAPES[shape][6]
     prompts = torch.from_numpy(W.prompts(n_prompts, P, V)).to(dev)
     logits = torch.empty((S, V), dtype=torch.float32, device=dev)
