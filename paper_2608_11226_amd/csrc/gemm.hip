@@ -699,22 +699,44 @@ hipError_t launch_tile(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, floa
   return hipGetLastError();
 }
 
-// Ring kernel shape: weight blocks per wave and K slices, aiming at ~512 waves with K slices of at least
-// 256 (gate/up with SwiGLU: 4 blocks, one split).  A grid short of the target runs two waves per
-// workgroup, each taking half of the workgroup's K slice, so a projection that needs many K slices for
-// its waves writes half as many partials (its consumers sum half as many) and its waves run as fast or
-// faster (7B decode: QKV 11.6 -> 10.8 us, down 28.4 -> 27.1 us; summing the partials 8.5 -> 5.2 us).
+// Ring kernel shape of the split projections (QKV, O, down at M <= 64).  Workgroups of 4 or 8 weight
+// blocks, K split just far enough that the grid fills 80% of the CUs with at most one workgroup per CU: a
+// CU's streaming rate bounds these kernels, so a second workgroup on some CUs sets the time, while every
+// further split adds a partial for the consumer to sum.  Four-block workgroups are taken when their grid fills at least 80% of the CUs with K
+// slices of at most 4096 (their activation reads per weight byte are twice those of eight blocks, which
+// costs more than it saves on long K slices); their waves split the K slice four ways while each keeps at
+// least 8 k-steps, else two.  Eight-block workgroups run two waves (one when the grid already holds two
+// workgroups per CU).  A sweep over blocks per wave (2, 4, 8), waves per workgroup (1, 2, 4) and 1-16
+// splits at M = 64 (GEMM time plus reading the partials) puts the optimum at this rule for the 7B and
+// 72B QKV, O and down shapes: 7B O 10.3 -> 9.3 us with 4 instead of 7 partials, QKV 11.4 -> 10.5 us with
+// 3 instead of 7, 72B O 28.1 -> 26.1 us with 2 instead of 4; the two down projections keep 8 blocks.
+// Gate/up with SwiGLU (one split) and the LM head take the balanced grids below.
 constexpr int kRingMaxRows = 64;
 constexpr int kRingTargetWaves = 512;
 int ring_groups(int N, int nbw) { return (N / 16 + nbw - 1) / nbw; }
+bool ring_four_blocks(int N, int K, int splits) {
+  const int g = ring_groups(N, 4) * splits, cus = device_cus();
+  return g <= cus && 5 * g >= 4 * cus && kslice_for(K, splits) <= 4096;
+}
 int ring_splits(int N, int K, int max_splits) {
-  const int groups = ring_groups(N, 8);
-  int s = (kRingTargetWaves + groups - 1) / groups;  // K slices of one wave
-  s = std::min(s, std::max(1, K / 256));
-  s = std::max(1, std::min(s, max_splits));
-  if (s >= 2) s = (s + 1) / 2;                        // two waves per workgroup
-  const int ks = kslice_for(K, s);
-  return (K + ks - 1) / ks;
+  const int cus = device_cus();
+  const int smax = std::max(1, std::min(max_splits, K / 256));
+  // the fewest splits that bring a grid of g workgroups to 80% of the CUs, never past one per CU
+  auto pick = [&](int g) {
+    int s = (4 * cus + 5 * g - 1) / (5 * g);
+    if (s * g > cus) s = cus / g;
+    s = std::max(1, std::min(smax, s));
+    const int ks = kslice_for(K, s);
+    return (K + ks - 1) / ks;
+  };
+  const int s4 = pick(ring_groups(N, 4));
+  if (ring_four_blocks(N, K, s4)) return s4;
+  return pick(ring_groups(N, 8));
+}
+// waves per workgroup of a split projection's ring kernel with nbw blocks
+int ring_split_waves(int N, int K, int nbw, int splits) {
+  if (nbw == 4) return kslice_for(K, splits) / 32 / 4 >= 8 ? 4 : 2;
+  return ring_groups(N, nbw) * splits < 2 * device_cus() ? 2 : 1;
 }
 int ring_waves_per_group(int N, int nbw, int splits) {
   return ring_groups(N, nbw) * splits < kRingTargetWaves ? 2 : 1;
@@ -773,6 +795,23 @@ hipError_t launch_ring(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, floa
     launch_ring_kw<NBW, SWI, 2>(s, x, w, out, M, N, K, splits, h);
   else
     launch_ring_kw<NBW, SWI, 1>(s, x, w, out, M, N, K, splits, h);
+  return hipGetLastError();
+}
+
+// A split projection (no SwiGLU) on the ring kernel, shaped by ring_four_blocks / ring_split_waves.  Any
+// shape gives the same partials; the split count is the caller's.
+hipError_t launch_ring_split(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
+                             int splits) {
+  if (ring_four_blocks(N, K, splits)) {
+    if (ring_split_waves(N, K, 4, splits) == 4)
+      launch_ring_kw<4, false, 4>(s, x, w, out, M, N, K, splits, nullptr);
+    else
+      launch_ring_kw<4, false, 2>(s, x, w, out, M, N, K, splits, nullptr);
+  } else if (ring_split_waves(N, K, 8, splits) == 2) {
+    launch_ring_kw<8, false, 2>(s, x, w, out, M, N, K, splits, nullptr);
+  } else {
+    launch_ring_kw<8, false, 1>(s, x, w, out, M, N, K, splits, nullptr);
+  }
   return hipGetLastError();
 }
 
@@ -878,7 +917,7 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* X, int ldx, const v
   if (M <= kRingMaxRows) {
     if (use_balanced_single(M, N, splits))
       return launch_ring_balanced<false, 1>(s, x, w, out, M, N, K, kBalWavesPerCU * device_cus(), nullptr);
-    return launch_ring<8, false>(s, x, w, out, M, N, K, splits, nullptr);
+    return launch_ring_split(s, x, w, out, M, N, K, splits);
   }
   return launch_tile(s, x, w, out, M, N, K, splits);
 }
