@@ -705,11 +705,12 @@ hipError_t launch_tile(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, floa
 // further split adds a partial for the consumer to sum.  Four-block workgroups are taken when their grid fills at least 80% of the CUs with K
 // slices of at most 4096 (their activation reads per weight byte are twice those of eight blocks, which
 // costs more than it saves on long K slices); their waves split the K slice four ways while each keeps at
-// least 8 k-steps, else two.  Eight-block workgroups run two waves (one when the grid already holds two
+// least 6 k-steps, else two.  Eight-block workgroups run two waves (one when the grid already holds two
 // workgroups per CU).  A sweep over blocks per wave (2, 4, 8), waves per workgroup (1, 2, 4) and 1-16
 // splits at M = 64 (GEMM time plus reading the partials) puts the optimum at this rule for the 7B and
-// 72B QKV, O and down shapes: 7B O 10.3 -> 9.3 us with 4 instead of 7 partials, QKV 11.4 -> 10.5 us with
-// 3 instead of 7, 72B O 28.1 -> 26.1 us with 2 instead of 4; the two down projections keep 8 blocks.
+// 72B QKV, O and down shapes (7B O 10.3 -> 9.3 us with 4 instead of 7 partials, QKV 11.4 -> 10.5 us with
+// 3 instead of 7, 72B O 28.1 -> 26.1 us with 2 instead of 4; the two down projections keep 8 blocks), and
+// the whole 7B rollout confirms it against the neighbouring shapes of each projection.
 // Gate/up with SwiGLU (one split) and the LM head take the balanced grids below.
 constexpr int kRingMaxRows = 64;
 constexpr int kRingTargetWaves = 512;
@@ -735,7 +736,7 @@ int ring_splits(int N, int K, int max_splits) {
 }
 // waves per workgroup of a split projection's ring kernel with nbw blocks
 int ring_split_waves(int N, int K, int nbw, int splits) {
-  if (nbw == 4) return kslice_for(K, splits) / 32 / 4 >= 8 ? 4 : 2;
+  if (nbw == 4) return kslice_for(K, splits) / 32 / 4 >= 6 ? 4 : 2;
   return ring_groups(N, nbw) * splits < 2 * device_cus() ? 2 : 1;
 }
 int ring_waves_per_group(int N, int nbw, int splits) {
