@@ -835,9 +835,8 @@ void launch_q4_mb(hipStream_t s, const bf16x8_t* x, const void* w, float* out, i
 }
 
 // Weight blocks per wave: 4 for up to two 16-row activation blocks, 2 above (registers: both fit two
-// waves per SIMD).  K splits aim at 512 workgroups, two per CU.
+// waves per SIMD).
 constexpr int q4_blocks(int M) { return M <= 32 ? 4 : 2; }
-constexpr int kQ4TargetWorkgroups = 512;
 
 template <bool SWI>
 hipError_t launch_q4(hipStream_t s, const bf16x8_t* x, const void* w, float* out, int M, int N, int K, int splits,
@@ -856,7 +855,11 @@ hipError_t launch_q4(hipStream_t s, const bf16x8_t* x, const void* w, float* out
 int gemm_splits_q4(int M, int N, int K, int max_splits) {
   if (M > kRingMaxRows || max_splits <= 1) return 1;
   const int groups = (N / 16 + 4 * q4_blocks(M) - 1) / (4 * q4_blocks(M));  // workgroups per K split
-  int s = (kQ4TargetWorkgroups + groups - 1) / groups;
+  // as for the bf16 split projections: the fewest splits that fill 80% of the CUs, at most one workgroup
+  // per CU (72B: QKV 3, O and down 4 instead of 7-8 splits at two workgroups per CU; 72B int4 rollout +1%)
+  const int cus = device_cus();
+  int s = (4 * cus + 5 * groups - 1) / (5 * groups);
+  if (s * groups > cus) s = cus / groups;
   s = std::min(s, std::max(1, K / 256));
   s = std::max(1, std::min(s, max_splits));
   const int ks = kslice_q4(K, s);
