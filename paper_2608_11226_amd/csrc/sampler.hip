@@ -20,9 +20,11 @@
 // pass over a row's V values runs as rows x chunks workgroups, a chunk being
 // a whole number of 4096-id batches that a workgroup loads in one round trip
 // (chunk max; exp stored once with the chunk mass and first-digit histogram; one
-// histogram pass per remaining digit; per-chunk kept mass and tie count);
-// between passes a small kernel per row picks the digit with a parallel
-// suffix scan over the 256 bins.  The final kernel per row scans the chunk
+// histogram pass per remaining digit; per-chunk kept mass and tie count).  The
+// chunks add their histogram bins into the row's histogram of each digit with
+// integer atomics (the same sums in any order), and every workgroup of the
+// next pass picks the digits chosen so far itself, with a parallel suffix scan
+// over the row's 256 bins per digit, so no pass waits for a selection kernel.  The final kernel per row scans the chunk
 // totals, finds the chunk holding the crossing, and walks only that chunk:
 // one contiguous segment per wave, segment totals scanned across waves, then
 // the crossing wave scans its segment 64 ids at a time.  Per row (128 rows
@@ -30,6 +32,7 @@
 #include "internal.h"
 
 #include <climits>
+#include <type_traits>
 #include <cstdlib>
 #include <string>
 
@@ -103,6 +106,109 @@ __device__ __forceinline__ u64 wave_incl_scan(u64 v, int lane) {
   return v;
 }
 
+// the row's mass histograms of the four digits (bits 24..31, 16..23, 8..15, 0..7), each over the values
+// that match the digits selected above it: rowhist[row][level][bin], level = (24 - shift) / 8
+constexpr int kLevels = 4;
+
+// Inclusive scan of one u64 per lane over the wave by DPP lane moves (no LDS): shifts of 1, 2, 4, 8 lanes
+// within each row of 16, then row 0's total into row 1 and row 2's into row 3 (row_bcast:15), then the
+// first two rows' total into rows 2 and 3 (row_bcast:31).  A lane with no source adds 0.
+__device__ __forceinline__ u64 wave_incl_scan_dpp(u64 v) {
+  auto step = [&](auto ctrl, auto row_mask) {
+    constexpr int c = decltype(ctrl)::value, r = decltype(row_mask)::value;
+    const unsigned lo = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)v, c, r, 0xf, false);
+    const unsigned hi = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)(v >> 32), c, r, 0xf, false);
+    v += ((u64)hi << 32) | lo;
+  };
+  step(std::integral_constant<int, 0x111>{}, std::integral_constant<int, 0xf>{});  // row_shr:1
+  step(std::integral_constant<int, 0x112>{}, std::integral_constant<int, 0xf>{});  // row_shr:2
+  step(std::integral_constant<int, 0x114>{}, std::integral_constant<int, 0xf>{});  // row_shr:4
+  step(std::integral_constant<int, 0x118>{}, std::integral_constant<int, 0xf>{});  // row_shr:8
+  step(std::integral_constant<int, 0x142>{}, std::integral_constant<int, 0xa>{});  // row_bcast:15
+  step(std::integral_constant<int, 0x143>{}, std::integral_constant<int, 0xc>{});  // row_bcast:31
+  return v;
+}
+
+__device__ __forceinline__ u64 readlane_u64(u64 v, int lane) {
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)v, lane);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v >> 32), lane);
+  return ((u64)hi << 32) | lo;
+}
+
+// Row state before the first digit, from the first digit's bins (lane l: h[k] = bin 255 - 4l - k): total
+// mass and the mass the kept set must reach.
+__device__ __forceinline__ RowSel select_init(const u64* h, float top_p) {
+  const u64 total = readlane_u64(wave_incl_scan_dpp(h[0] + h[1] + h[2] + h[3]), 63);
+  RowSel st;
+  st.total = total;
+  const u64 target = (u64)ceil((double)top_p * (double)total);
+  st.target = target > total ? total : (target == 0 ? 1 : target);
+  st.above = 0;
+  st.prefix = 0;
+  st.mask = 0;
+  st.kties = 0;
+  st.kept = 0;
+  st.m = 0.f;
+  st.pad = 0;
+  return st;
+}
+
+// One digit of the selection, by one wave: lane l holds h[k] = bin 255 - 4l - k (k = 0..3) of the row's
+// histogram at `shift`.  The digit is the largest d with above + sum_{j >= d} hist[j] >= target: suffix
+// sums in descending digit order (within the lane, then across lanes by a scan), the first place where
+// they reach the target.  At the last digit also the kept ties and the kept mass.  Every wave of every
+// workgroup of a row computes the same integers, so no wave waits for another.
+__device__ __forceinline__ void select_digit(const u64* h, int shift, RowSel& st) {
+  const u64 c0 = h[0], c1 = c0 + h[1], c2 = c1 + h[2], c3 = c2 + h[3];
+  const u64 excl = wave_incl_scan_dpp(c3) - c3;  // mass of the digits of the lanes before this one
+  const bool r0 = st.above + excl + c0 >= st.target, r1 = st.above + excl + c1 >= st.target,
+             r2 = st.above + excl + c2 >= st.target, r3 = st.above + excl + c3 >= st.target;
+  const unsigned long long bal = __ballot(r3);
+  if (!bal) return;
+  const int first = __ffsll((long long)bal) - 1;  // the lane holding the selected digit
+  const int k = r0 ? 0 : (r1 ? 1 : (r2 ? 2 : 3));
+  const u64 ck = r0 ? c0 : (r1 ? c1 : (r2 ? c2 : c3));
+  const u64 hk = r0 ? h[0] : (r1 ? h[1] : (r2 ? h[2] : h[3]));
+  const int dsel = 255 - 4 * first - __builtin_amdgcn_readlane(k, first);
+  st.above = readlane_u64(st.above + excl + ck - hk, first);  // mass of the digits above dsel
+  st.prefix |= (unsigned)dsel << shift;
+  st.mask |= 255u << shift;
+  if (shift == 0) {
+    const u64 ftau = fx40(__uint_as_float(st.prefix));
+    const u64 need = st.target - st.above;
+    st.kties = ftau ? (need + ftau - 1) / ftau : 0;
+    st.kept = st.above + st.kties * ftau;
+  }
+}
+
+// this lane's bins of the row histograms at levels 0 .. kLevels - 1 (level l clamped to lmax)
+__device__ __forceinline__ void load_row_bins(const u64* __restrict__ rh, int lmax, u64 (*hb)[4]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) hb[l][k] = rh[min(l, lmax) * 256 + 255 - 4 * lane - k];
+}
+
+// The row state after the digits of levels 0 .. levels - 1, selected again by every wave from the row
+// histograms (a few scans; cheaper than a round trip to state left by the previous pass)
+__device__ __forceinline__ RowSel select_above(const u64 (*hb)[4], int levels, float top_p) {
+  RowSel st = select_init(hb[0], top_p);
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l)
+    if (l < levels) select_digit(hb[l], 24 - 8 * l, st);
+  return st;
+}
+
+// A chunk's digit histogram into the row's: thread t adds bin t of its waves' LDS copies (bins with no
+// mass are skipped)
+__device__ __forceinline__ void add_row_bins(u64 (*hist)[256], u64* __restrict__ rh) {
+  u64 t = 0;
+#pragma unroll
+  for (int j = 0; j < CW; ++j) t += hist[j][threadIdx.x];
+  if (t) atomicAdd(rh + threadIdx.x, t);
+}
+
 // ---------------------------------------------------------------------------
 // greedy
 // ---------------------------------------------------------------------------
@@ -156,9 +262,11 @@ __global__ __launch_bounds__(64) void k_argmax_final(const float* __restrict__ c
 // ---------------------------------------------------------------------------
 // cmax[row][c] = max over chunk c of fp32(z / T)
 __global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logits, int V, int chunk, float T,
-                                                  float* __restrict__ cmax) {
+                                                  float* __restrict__ cmax, u64* __restrict__ rowhist) {
   __shared__ float red[CW];
   const int row = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
+  if (c == 0)  // the row's digit histograms start from zero in every call
+    for (int i = tid; i < kLevels * 256; i += CB) rowhist[(size_t)row * kLevels * 256 + i] = 0;
   const float* z = logits + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
   float mx = -INFINITY;
@@ -180,7 +288,7 @@ __global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logi
 // e = exp(y - m) stored; chunk mass; first-digit (bits 24..31) mass histogram when filtering
 __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logits, int V, int chunk, float T,
                                                   const float* __restrict__ cmax, float* __restrict__ escr,
-                                                  u64* __restrict__ cmass, u64* __restrict__ chist, int filter) {
+                                                  u64* __restrict__ cmass, u64* __restrict__ rowhist, int filter) {
   __shared__ u64 hist[CW][256];
   __shared__ u64 red[CW];
   const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
@@ -216,112 +324,69 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
     for (int j = 0; j < CW; ++j) t += red[j];
     cmass[(size_t)row * nc + c] = t;
   }
-  if (filter) {
-    u64 t = 0;
-    for (int j = 0; j < CW; ++j) t += hist[j][tid];
-    chist[((size_t)row * nc + c) * 256 + tid] = t;
-  }
+  if (filter) add_row_bins(hist, rowhist + (size_t)row * kLevels * 256);
 }
 
-// Pick the digit at `shift`: the largest d with above + sum_{j >= d} hist[j] >= target.
-// One workgroup of 256 threads per row; thread t owns digit 255 - t for the suffix scan.
-__global__ __launch_bounds__(256) void k_select_digit(const u64* __restrict__ chist, const u64* __restrict__ cmass,
-                                                      int nc, float top_p, int shift, RowSel* __restrict__ sel) {
-  __shared__ u64 wtot[4];
-  __shared__ int wcnt[4];
-  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  RowSel st = sel[row];
-  if (shift == 24) {  // first digit: initialise the row state from the chunk masses
-    u64 total = 0;
-    {
-      u64 mv[kMaxChunks];
-#pragma unroll
-      for (int j = 0; j < kMaxChunks; ++j) mv[j] = cmass[(size_t)row * nc + min(j, nc - 1)];
-#pragma unroll
-      for (int j = 0; j < kMaxChunks; ++j)
-        if (j < nc) total += mv[j];
-    }
-    st.total = total;
-    u64 target = (u64)ceil((double)top_p * (double)total);
-    st.target = target > total ? total : (target == 0 ? 1 : target);
-    st.above = 0;
-    st.prefix = 0;
-    st.mask = 0;
-  }
-  const int d = 255 - tid;
-  u64 h = 0;
-  {
-    // all nc chunk counts in flight at once (nc <= kMaxChunks; indices clamped, surplus masked)
-    u64 hv[kMaxChunks];
-#pragma unroll
-    for (int j = 0; j < kMaxChunks; ++j) hv[j] = chist[((size_t)row * nc + min(j, nc - 1)) * 256 + d];
-#pragma unroll
-    for (int j = 0; j < kMaxChunks; ++j)
-      if (j < nc) h += hv[j];
-  }
-  // inclusive scan in thread order = suffix sum over digits >= d
-  u64 inc = wave_incl_scan(h, lane);
-  if (lane == 63) wtot[w] = inc;
-  __syncthreads();
-  for (int j = 0; j < w; ++j) inc += wtot[j];
-  const bool reach = st.above + inc >= st.target;  // true exactly for digits 0 .. d*
-  const unsigned long long bal = __ballot(reach);
-  if (lane == 0) wcnt[w] = __popcll(bal);
-  __syncthreads();
-  // reach holds for threads tid >= 255 - d*, i.e. the count of true lanes is d* + 1
-  const int dsel = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3] - 1;
-  if (d == dsel) {
-    st.above = st.above + inc - h;  // mass of digits above dsel
-    st.prefix |= (unsigned)dsel << shift;
-    st.mask |= 255u << shift;
-    if (shift == 0) {
-      const u64 ftau = fx40(__uint_as_float(st.prefix));
-      const u64 need = st.target - st.above;
-      st.kties = ftau ? (need + ftau - 1) / ftau : 0;
-      st.kept = st.above + st.kties * ftau;
-    }
-    sel[row] = st;
-  }
-}
-
-// mass histogram of the digit at `shift` over values matching the selected prefix
+// mass histogram of the digit at `shift` over values matching the digits selected above it; each
+// workgroup first selects those digits from the row's histograms (the same integers in every workgroup)
 __global__ __launch_bounds__(CB) void k_chunk_hist(const float* __restrict__ escr, int V, int chunk, int shift,
-                                                   const RowSel* __restrict__ sel, u64* __restrict__ chist) {
+                                                   float top_p, u64* __restrict__ rowhist) {
   __shared__ u64 hist[CW][256];
-  const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
-  const unsigned prefix = sel[row].prefix, mask = sel[row].mask;
+  const int row = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
+  const int level = (24 - shift) >> 3;  // 1..3; the digits above are levels 0 .. level - 1
+  u64* rh = rowhist + (size_t)row * kLevels * 256;
   const float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
+  // this lane's bins of the digits above, then the chunk's first batch: waiting for the bins leaves the
+  // batch in flight during the selection
+  u64 hb[kLevels][4];
+  load_row_bins(rh, level - 1, hb);
+  float v[kPer];
+  load_batch(e_row, lo, hi, v);
   for (int i = tid; i < CW * 256; i += CB) (&hist[0][0])[i] = 0;
-  __syncthreads();
-  for (int b0 = lo; b0 < hi; b0 += kBatch) {
-    float v[kPer];
-    load_batch(e_row, b0, hi, v);
+  const RowSel st = select_above(hb, level, top_p);
+  const unsigned prefix = st.prefix, mask = st.mask;
+  __syncthreads();  // the cleared bins
+  auto add = [&](int b0) {
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const unsigned b = __float_as_uint(v[j]);
       if (b0 + j * CB + tid < hi && (b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(v[j]));
     }
+  };
+  add(lo);
+  for (int b0 = lo + kBatch; b0 < hi; b0 += kBatch) {
+    load_batch(e_row, b0, hi, v);
+    add(b0);
   }
   __syncthreads();
-  u64 t = 0;
-  for (int j = 0; j < CW; ++j) t += hist[j][tid];
-  chist[((size_t)row * nc + c) * 256 + tid] = t;
+  add_row_bins(hist, rh + level * 256);
 }
 
-// per chunk: mass of kept values strictly above tau (all values without filtering) and ties at tau
+// per chunk: mass of kept values strictly above tau (all values without filtering) and ties at tau; with
+// filtering each workgroup selects tau from the row's histograms first, and the chunk-0 workgroup leaves
+// the row's selection for the draw
 __global__ __launch_bounds__(CB) void k_chunk_kept(const float* __restrict__ escr, int V, int chunk, int filter,
-                                                   const RowSel* __restrict__ sel, u64* __restrict__ cgt,
+                                                   float top_p, const u64* __restrict__ rowhist,
+                                                   RowSel* __restrict__ sel, u64* __restrict__ cgt,
                                                    u64* __restrict__ cties) {
   __shared__ u64 r1[CW], r2[CW];
   const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
-  const unsigned tau = filter ? sel[row].prefix : 0u;
+  const u64* rh = rowhist + (size_t)row * kLevels * 256;
   const float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
+  u64 hb[kLevels][4];
+  load_row_bins(rh, kLevels - 1, hb);
+  float v[kPer];
+  load_batch(e_row, lo, hi, v);
+  unsigned tau = 0u;
+  if (filter) {
+    const RowSel st = select_above(hb, kLevels, top_p);
+    tau = st.prefix;
+    if (c == 0 && tid == 0) sel[row] = st;
+  }
   u64 gt = 0, ties = 0;
-  for (int b0 = lo; b0 < hi; b0 += kBatch) {
-    float v[kPer];
-    load_batch(e_row, b0, hi, v);
+  auto add = [&](int b0) {
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const bool ok = b0 + j * CB + tid < hi;
@@ -330,6 +395,11 @@ __global__ __launch_bounds__(CB) void k_chunk_kept(const float* __restrict__ esc
       gt += ok && (!filter || b > tau) ? f : 0ull;
       ties += ok && filter && b == tau ? 1ull : 0ull;
     }
+  };
+  add(lo);
+  for (int b0 = lo + kBatch; b0 < hi; b0 += kBatch) {
+    load_batch(e_row, b0, hi, v);
+    add(b0);
   }
   gt = wave_sum_u64(gt);
   ties = wave_sum_u64(ties);
@@ -751,7 +821,8 @@ int sample_chunks(int V) {
 
 size_t sample_scratch_bytes(int S, int V) {
   const int nc = sample_chunks(V);
-  return (size_t)S * V * 4 + (size_t)S * nc * (4 + 4 + 8 * 4 + 256 * 8) + (size_t)S * sizeof(RowSel) + 4096;
+  return (size_t)S * V * 4 + (size_t)S * nc * (4 + 4 + 8 * 3) + (size_t)S * kLevels * 256 * 8 +
+         (size_t)S * sizeof(RowSel) + 4096;
 }
 
 int sample_rows_fitting(size_t bytes, int V) {
@@ -782,7 +853,7 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
   u64* cmass = (u64*)take((size_t)S * nc * 8);
   u64* cgt = (u64*)take((size_t)S * nc * 8);
   u64* cties = (u64*)take((size_t)S * nc * 8);
-  u64* chist = (u64*)take((size_t)S * nc * 256 * 8);
+  u64* rowhist = (u64*)take((size_t)S * kLevels * 256 * 8);
   RowSel* sel = (RowSel*)take((size_t)S * sizeof(RowSel));
   const dim3 rc(S, nc);
   if (temperature == 0.0f) {
@@ -796,16 +867,13 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
                        col, out, out_stride);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax);
-  hipLaunchKernelGGL(k_chunk_exp, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass, chist,
+  hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, rowhist);
+  hipLaunchKernelGGL(k_chunk_exp, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass, rowhist,
                      filter);
-  if (filter) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      if (shift != 24) hipLaunchKernelGGL(k_chunk_hist, rc, dim3(CB), 0, s, escr, V, chunk, shift, sel, chist);
-      hipLaunchKernelGGL(k_select_digit, dim3(S), dim3(256), 0, s, chist, cmass, nc, top_p, shift, sel);
-    }
-  }
-  hipLaunchKernelGGL(k_chunk_kept, rc, dim3(CB), 0, s, escr, V, chunk, filter, sel, cgt, cties);
+  if (filter)
+    for (int shift = 16; shift >= 0; shift -= 8)
+      hipLaunchKernelGGL(k_chunk_hist, rc, dim3(CB), 0, s, escr, V, chunk, shift, top_p, rowhist);
+  hipLaunchKernelGGL(k_chunk_kept, rc, dim3(CB), 0, s, escr, V, chunk, filter, top_p, rowhist, sel, cgt, cties);
   hipLaunchKernelGGL(k_draw, dim3(S), dim3(RB), 0, s, escr, V, chunk, nc, filter, sel, cgt, cties, cmass, u,
                      u_stride, col, out, out_stride);
   return hipGetLastError();

@@ -46,9 +46,10 @@ def test_noalloc_draw_equals_rollout_sample_twice_the_second_smaller(V, T, top_p
 
 @pytest.mark.gpu
 def test_noalloc_draw_in_several_batches_of_the_fixed_scratch():
-    # 152064 logits per row: the 64 MiB scratch holds 97 rows, so 200 rows take three batches
+    # 152064 logits per row (38 chunks): exp values, five words per chunk and four 256-bin digit histograms
+    # per row -- the 64 MiB scratch holds 108 rows, so 200 rows take two batches
     V, S = 152064, 200
-    per_row = 4 * V + 38 * 2088 + 56
+    per_row = 4 * V + 38 * 32 + 4 * 256 * 8 + 56
     assert (R.NOALLOC_SCRATCH_BYTES - 4096) // per_row < S
     print(f"noalloc sampler V={V}: {S} rows in batches", flush=True)
     got, want = _draw_both(V, S, 0.9, 0.95, 11)
@@ -91,7 +92,7 @@ def test_noalloc_validates_before_any_device_work():
     # fake (never dereferenced) addresses: every error below is raised before the device is touched
     fake = 1 << 20
     with pytest.raises(R.RolloutError, match="ENOMEM"):
-        R.rollout_sample_noalloc(fake, 1, 16_742_771, 1.0, 1.0, fake, fake)
+        R.rollout_sample_noalloc(fake, 1, 1 << 24, 1.0, 1.0, fake, fake)  # 64 MiB of exp values alone
     for args in ((0, 1, 1024, 1.0, 1.0, fake, fake), (fake, 0, 1024, 1.0, 1.0, fake, fake),
                  (fake, 1, 1, 1.0, 1.0, fake, fake), (fake, 1, 1024, -1.0, 1.0, fake, fake),
                  (fake, 1, 1024, 1.0, 0.0, fake, fake), (fake, 1, 1024, 1.0, 1.5, fake, fake)):
