@@ -260,8 +260,9 @@ __global__ __launch_bounds__(64) void k_argmax_final(const float* __restrict__ c
 // ---------------------------------------------------------------------------
 // sampling
 // ---------------------------------------------------------------------------
-// cmax[row][c] = max over chunk c of fp32(z / T)
-__global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logits, int V, int chunk, float T,
+// cmax[row][c] = max over chunk c of z.  For T > 0 the rounded quotient fp32(z / T) does not decrease as
+// z grows, so the largest y of the row is fp32(max z / T): the exp pass divides the row maximum once.
+__global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logits, int V, int chunk,
                                                   float* __restrict__ cmax, u64* __restrict__ rowhist) {
   __shared__ float red[CW];
   const int row = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
@@ -274,7 +275,7 @@ __global__ __launch_bounds__(CB) void k_chunk_max(const float* __restrict__ logi
     float v[kPer];
     load_batch(z, b, hi, v);
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) mx = fmaxf(mx, b + j * CB + tid < hi ? v[j] / T : -INFINITY);
+    for (int j = 0; j < kPer; ++j) mx = fmaxf(mx, b + j * CB + tid < hi ? v[j] : -INFINITY);
   }
   mx = wave_max(mx);
   if ((tid & 63) == 0) red[tid >> 6] = mx;
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
   __shared__ u64 hist[CW][256];
   __shared__ u64 red[CW];
   const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
-  const float m = row_max(cmax + (size_t)row * nc, nc);
+  const float m = row_max(cmax + (size_t)row * nc, nc) / T;  // max of fp32(z / T) (see k_chunk_max)
   const float* z = logits + (size_t)row * V;
   float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
@@ -867,7 +868,7 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
                        col, out, out_stride);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, rowhist);
+  hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, cmax, rowhist);
   hipLaunchKernelGGL(k_chunk_exp, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass, rowhist,
                      filter);
   if (filter)
