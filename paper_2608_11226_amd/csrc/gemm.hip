@@ -764,27 +764,36 @@ void launch_ring_kw(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* 
 // The same balance for single-split projections of many blocks (the LM head): four one-wave workgroups per
 // CU, each with floor(nbt / grid) or one more of the blocks (7B: 9 or 10 instead of 1188 eight-block
 // workgroups, 4.6 per CU; LM head 199.7 -> 180.4 us in isolation).
+// Gate/up with more than kBalNBW blocks per CU (72B: 3,696 blocks, 14.4 per CU) takes two one-wave
+// workgroups per CU with up to kBal2NBW blocks each, every wave streaming its blocks over the whole K:
+// the one-wave-per-four-blocks grid put four workgroups on 156 CUs and three on 100 (72B rollout 2,176 ->
+// 2,284 tokens/s; two two-wave workgroups per CU 2,264, four one-wave workgroups per CU 2,146).
 constexpr int kBalNBW = 10;
+constexpr int kBal2NBW = 8;
 constexpr int kBalWavesPerCU = 4;
 bool use_balanced_swiglu(int M, int N) {
   const int nbt = N / 16, cus = device_cus();
   return M <= kRingMaxRows && nbt >= 4 * cus && nbt <= kBalNBW * cus;
+}
+bool use_balanced_swiglu_wide(int M, int N) {
+  const int nbt = N / 16, cus = device_cus();
+  return M <= kRingMaxRows && nbt > kBalNBW * cus && nbt <= 2 * kBal2NBW * cus;
 }
 bool use_balanced_single(int M, int N, int splits) {
   const int nbt = N / 16, g = kBalWavesPerCU * device_cus();
   return M <= kRingMaxRows && splits == 1 && nbt >= 4 * g && nbt <= kBalNBW * g;
 }
 
-template <bool SWI, int KW>
+template <bool SWI, int KW, int NBW = kBalNBW>
 hipError_t launch_ring_balanced(hipStream_t s, const bf16x8_t* x, const bf16x8_t* w, float* out, int M, int N, int K,
                                 int groups, uint16_t* h) {
   const int kslice = kslice_for(K, 1);
   const dim3 grid(groups, 1), block(64 * KW);
   switch ((M + 15) / 16) {
-    case 1: hipLaunchKernelGGL((k_gemm_ring<1, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    case 2: hipLaunchKernelGGL((k_gemm_ring<2, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    case 3: hipLaunchKernelGGL((k_gemm_ring<3, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
-    default: hipLaunchKernelGGL((k_gemm_ring<4, kBalNBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 1: hipLaunchKernelGGL((k_gemm_ring<1, NBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 2: hipLaunchKernelGGL((k_gemm_ring<2, NBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    case 3: hipLaunchKernelGGL((k_gemm_ring<3, NBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
+    default: hipLaunchKernelGGL((k_gemm_ring<4, NBW, 2, SWI, KW, true>), grid, block, 0, s, x, w, out, M, N, K, kslice, h); break;
   }
   return hipGetLastError();
 }
@@ -936,6 +945,9 @@ hipError_t launch_gemm_swiglu(hipStream_t s, const void* X, const void* W, int M
   if (use_balanced_swiglu(M, N))
     return launch_ring_balanced<true, 2>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, device_cus(),
                                          (uint16_t*)h);
+  if (use_balanced_swiglu_wide(M, N))
+    return launch_ring_balanced<true, 1, kBal2NBW>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K,
+                                                   2 * device_cus(), (uint16_t*)h);
   return launch_ring<4, true>(s, (const bf16x8_t*)X, (const bf16x8_t*)W, nullptr, M, N, K, 1, (uint16_t*)h);
 }
 
