@@ -254,8 +254,9 @@ struct AttnQKV {
 
 // ONE: every column group of the q/k/v formation fits one per thread ((nrep + 2) * HD / 4 <= NW * 64), so
 // the partials of a single group are held (fewer registers, more workgroups per CU); else up to 16 query
-// heads per KV head.
-template <int HD, int NW, int DR, bool FQ, bool SPLIT = false, bool ONE = false>
+// heads per KV head.  QBX: QKV split partials loaded with the block table (0: kQkvBatch, half for ONE); the
+// launch takes 4 when the QKV projection has at most 4 splits, so no loads are spent on surplus partials.
+template <int HD, int NW, int DR, bool FQ, bool SPLIT = false, bool ONE = false, int QBX = 0>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(ONE && NW == 4 ? 3 : 1)))
 void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
                                                        uint16_t* __restrict__ kv, int n_blocks,
@@ -304,7 +305,7 @@ void k_attn_mfma(Dims D, const uint16_t* __restrict__ q,
   // the waits on the partials (and the LDS-only barriers after them) leave the tile loads in flight.
   const int ntab = (t_end + blk - 1) / blk;
   constexpr int GI = ONE ? 1 : (18 * (HD / 4) + NT - 1) / NT;  // column groups per thread (nrep <= 16)
-  constexpr int QB = ONE ? kQkvBatch / 2 : kQkvBatch;              // partials loaded with the table
+  constexpr int QB = QBX ? QBX : (ONE ? kQkvBatch / 2 : kQkvBatch);  // partials loaded with the table
   const int ng = (nrep + 2) * (HD / 4);
   const float* pr = FQ ? Q.part + (size_t)r * D.nqkv : nullptr;
   const size_t split_stride = (size_t)R * D.nqkv;
@@ -887,6 +888,13 @@ hipError_t launch_attention(hipStream_t s, const Dims& D, const void* q, void* k
       if (one_group(D, NW)) {                                                                                          \
         hipLaunchKernelGGL((k_attn_mfma<HD, NW, DR, FQ, false, true>), grid, dim3(NW * 64), tab_bytes, s, D, qq, kk,   \
                            n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err);                                    \
+        break;                                                                                                         \
+      }                                                                                                                \
+    }                                                                                                                  \
+    if constexpr (FQ && DR == 2 && NW == 4) {                                                                      \
+      if (qkv_splits <= 4) {                                                                                           \
+        hipLaunchKernelGGL((k_attn_mfma<HD, NW, DR, FQ, false, false, 4>), grid, dim3(NW * 64), tab_bytes, s, D, qq,   \
+                           kk, n_blocks, tables, max_blocks, rm, R, layer, Q, oo, err);                                \
         break;                                                                                                         \
       }                                                                                                                \
     }                                                                                                                  \
