@@ -335,6 +335,7 @@ hipError_t launch_residual_norm(hipStream_t s, int dtype, const float* part, int
                          eps, (float*)out);                                                                           \
   } while (0)
     if (!part || splits <= 1) ROLLOUT_NORM_ROW(1);
+    else if (splits <= 2) ROLLOUT_NORM_ROW(2);
     else if (splits <= 4) ROLLOUT_NORM_ROW(4);
     else ROLLOUT_NORM_ROW(8);
 #undef ROLLOUT_NORM_ROW
