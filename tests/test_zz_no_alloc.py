@@ -91,8 +91,13 @@ def test_noalloc_draw_matches_the_oracle_at_vocabularies_no_context_has(V, T, to
 def test_noalloc_validates_before_any_device_work():
     # fake (never dereferenced) addresses: every error below is raised before the device is touched
     fake = 1 << 20
+    # the largest row the 64 MiB scratch holds: 16,773,618 exp values, 64 chunks of five words, four 256-bin
+    # histograms, the row's selection and 4 KiB of alignment slack; one logit more is rejected
     with pytest.raises(R.RolloutError, match="ENOMEM"):
-        R.rollout_sample_noalloc(fake, 1, 1 << 24, 1.0, 1.0, fake, fake)  # 64 MiB of exp values alone
+        R.rollout_sample_noalloc(fake, 1, 16_773_619, 1.0, 1.0, fake, fake)
+    assert "16773619 logits" in R.rollout_last_error()
+    with pytest.raises(R.RolloutError, match="ENOMEM"):
+        R.rollout_sample_noalloc(fake, 1, 1 << 24, 1.0, 1.0, fake, fake)
     for args in ((0, 1, 1024, 1.0, 1.0, fake, fake), (fake, 0, 1024, 1.0, 1.0, fake, fake),
                  (fake, 1, 1, 1.0, 1.0, fake, fake), (fake, 1, 1024, -1.0, 1.0, fake, fake),
                  (fake, 1, 1024, 1.0, 0.0, fake, fake), (fake, 1, 1024, 1.0, 1.5, fake, fake)):
