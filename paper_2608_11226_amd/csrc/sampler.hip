@@ -27,8 +27,9 @@
 // over the row's 256 bins per digit, so no pass waits for a selection kernel.  The final kernel per row scans the chunk
 // totals, finds the chunk holding the crossing, and walks only that chunk:
 // one contiguous segment per wave, segment totals scanned across waves, then
-// the crossing wave scans its segment 64 ids at a time.  Per row (128 rows
-// and more): one workgroup makes all of these passes over its row.
+// the crossing wave scans its segment 64 ids at a time.  Per row (from 128
+// rows without top-p filtering, from 256 with it): one workgroup makes all of
+// these passes over its row.
 #include "internal.h"
 
 #include <climits>
@@ -791,19 +792,19 @@ __global__ __launch_bounds__(SR) void k_sample_row(const float* __restrict__ log
   if (tid == 0) out[(size_t)row * out_stride + c_out] = s_tok < 0 ? 0 : s_tok;
 }
 
-// Which path samples S rows: one workgroup per row once there are kRowMinRows rows or more (its time is
+// Which path samples S rows: one workgroup per row from a row count that depends on filtering (its time is
 // set by one workgroup's passes over its row, so it barely grows with S; the chunked kernels grow with S
-// and win below).  Measured at V = 152064, row / chunked: S = 64, top-p 0.95: 208 / 147 us, top-p 1:
-// 79 / 75 us; S = 128: 211 / 205 and 80 / 108 us; S = 256: 248 / 375 and 92 / 226 us.
-// ROLLOUT_SAMPLE_PATH=row or =chunked
-// forces a path (read per call; the row path still needs V % 4 == 0 and V <= kRowMaxV).
-constexpr int kRowMinRows = 128;
-bool use_row_sampler(int S, int V) {
+// and win below).  Measured at V = 152064, row / chunked: top-p 0.95: S = 64: 206 / 94 us, S = 128:
+// 210 / 147 us, S = 256: 245 / 258 us; top-p 1 (no digit passes): S = 64: 79 / 60 us, S = 128: 80 / 88 us,
+// S = 256: 90 / 152 us.  ROLLOUT_SAMPLE_PATH=row or =chunked forces a path (read per call; the row path
+// still needs V % 4 == 0 and V <= kRowMaxV).
+constexpr int kRowMinRows = 128, kRowMinRowsFiltered = 256;
+bool use_row_sampler(int S, int V, bool filter) {
   if (V % 4 != 0 || V > kRowMaxV) return false;
   const char* v = std::getenv("ROLLOUT_SAMPLE_PATH");
   if (v && std::string(v) == "row") return true;
   if (v && std::string(v) == "chunked") return false;
-  return S >= kRowMinRows;
+  return S >= (filter ? kRowMinRowsFiltered : kRowMinRows);
 }
 
 }  // namespace
@@ -863,7 +864,7 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
     return hipGetLastError();
   }
   const int filter = top_p < 1.0f;
-  if (use_row_sampler(S, V)) {
+  if (use_row_sampler(S, V, filter)) {
     hipLaunchKernelGGL(k_sample_row, dim3(S), dim3(SR), 0, s, logits, V, temperature, top_p, filter, escr, u, u_stride,
                        col, out, out_stride);
     return hipGetLastError();
