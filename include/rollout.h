@@ -274,7 +274,7 @@ const char* rollout_last_error(const rollout_ctx* ctx);
  * caller.  Errors (message from rollout_last_error(NULL)): EINVAL (NULL
  * buffer, n_seqs < 1, vocab < 2, temperature < 0, top_p outside (0, 1], a
  * stream of another device), ENOMEM (one row needs more scratch than the
- * array holds: vocab above 16,773,618), EDEVICE.
+ * array holds: vocab above 16,724,608), EDEVICE.
  */
 #define ROLLOUT_SAMPLE_NOALLOC_SCRATCH_BYTES (64ull << 20)
 rollout_status rollout_sample_noalloc(const float* d_logits, int32_t n_seqs, int32_t vocab, float temperature,

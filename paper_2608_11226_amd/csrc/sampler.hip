@@ -20,12 +20,14 @@
 // pass over a row's V values runs as rows x chunks workgroups, a chunk being
 // a whole number of 4096-id batches that a workgroup loads in one round trip
 // (chunk max; exp stored once with the chunk mass and first-digit histogram; one
-// histogram pass per remaining digit; per-chunk kept mass and tie count).  The
-// chunks add their histogram bins into the row's histogram of each digit with
-// integer atomics (the same sums in any order), and every workgroup of the
+// histogram pass per remaining digit, the last one also leaving per chunk what
+// its kept mass and its ties at tau are for either choice of the last digit).
+// The chunks add their histogram bins into the row's histogram of each digit
+// with integer atomics (the same sums in any order), and every workgroup of the
 // next pass picks the digits chosen so far itself, with a parallel suffix scan
-// over the row's 256 bins per digit, so no pass waits for a selection kernel.  The final kernel per row scans the chunk
-// totals, finds the chunk holding the crossing, and walks only that chunk:
+// over the row's 256 bins per digit, so no pass waits for a selection kernel.
+// The final kernel per row selects tau the same way, takes the chunks' kept
+// masses, finds the chunk holding the crossing, and walks only that chunk:
 // one contiguous segment per wave, segment totals scanned across waves, then
 // the crossing wave scans its segment 64 ids at a time.  Per row (from 128
 // rows without top-p filtering, from 256 with it): one workgroup makes all of
@@ -330,11 +332,20 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
 }
 
 // mass histogram of the digit at `shift` over values matching the digits selected above it; each
-// workgroup first selects those digits from the row's histograms (the same integers in every workgroup)
+// workgroup first selects those digits from the row's histograms (the same integers in every workgroup).
+// LAST (the lowest digit, shift 0): the chunk also leaves what the draw needs to find its kept mass once
+// the digit is chosen: the mass of its values above the selected 24-bit prefix (cabove), the suffix sums
+// of its own digit histogram (csuf[d] = mass of its matching values with digit >= d) and its count per
+// digit (ccnt), so the kept mass of the chunk is cabove + csuf[tau's digit + 1] and its ties at tau are
+// ccnt[tau's digit].
+template <bool LAST>
 __global__ __launch_bounds__(CB) void k_chunk_hist(const float* __restrict__ escr, int V, int chunk, int shift,
-                                                   float top_p, u64* __restrict__ rowhist) {
+                                                   float top_p, u64* __restrict__ rowhist, u64* __restrict__ cabove,
+                                                   u64* __restrict__ csuf, unsigned* __restrict__ ccnt) {
   __shared__ u64 hist[CW][256];
-  const int row = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
+  __shared__ unsigned cnt[LAST ? CW : 1][LAST ? 256 : 1];
+  __shared__ u64 red[CW];
+  const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int level = (24 - shift) >> 3;  // 1..3; the digits above are levels 0 .. level - 1
   u64* rh = rowhist + (size_t)row * kLevels * 256;
   const float* e_row = escr + (size_t)row * V;
@@ -346,56 +357,22 @@ __global__ __launch_bounds__(CB) void k_chunk_hist(const float* __restrict__ esc
   float v[kPer];
   load_batch(e_row, lo, hi, v);
   for (int i = tid; i < CW * 256; i += CB) (&hist[0][0])[i] = 0;
+  if constexpr (LAST)
+    for (int i = tid; i < CW * 256; i += CB) (&cnt[0][0])[i] = 0;
   const RowSel st = select_above(hb, level, top_p);
   const unsigned prefix = st.prefix, mask = st.mask;
   __syncthreads();  // the cleared bins
+  u64 above = 0;
   auto add = [&](int b0) {
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const unsigned b = __float_as_uint(v[j]);
-      if (b0 + j * CB + tid < hi && (b & mask) == prefix) atomicAdd(&hist[w][(b >> shift) & 255u], fx40(v[j]));
-    }
-  };
-  add(lo);
-  for (int b0 = lo + kBatch; b0 < hi; b0 += kBatch) {
-    load_batch(e_row, b0, hi, v);
-    add(b0);
-  }
-  __syncthreads();
-  add_row_bins(hist, rh + level * 256);
-}
-
-// per chunk: mass of kept values strictly above tau (all values without filtering) and ties at tau; with
-// filtering each workgroup selects tau from the row's histograms first, and the chunk-0 workgroup leaves
-// the row's selection for the draw
-__global__ __launch_bounds__(CB) void k_chunk_kept(const float* __restrict__ escr, int V, int chunk, int filter,
-                                                   float top_p, const u64* __restrict__ rowhist,
-                                                   RowSel* __restrict__ sel, u64* __restrict__ cgt,
-                                                   u64* __restrict__ cties) {
-  __shared__ u64 r1[CW], r2[CW];
-  const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
-  const u64* rh = rowhist + (size_t)row * kLevels * 256;
-  const float* e_row = escr + (size_t)row * V;
-  const int lo = c * chunk, hi = min(V, lo + chunk);
-  u64 hb[kLevels][4];
-  load_row_bins(rh, kLevels - 1, hb);
-  float v[kPer];
-  load_batch(e_row, lo, hi, v);
-  unsigned tau = 0u;
-  if (filter) {
-    const RowSel st = select_above(hb, kLevels, top_p);
-    tau = st.prefix;
-    if (c == 0 && tid == 0) sel[row] = st;
-  }
-  u64 gt = 0, ties = 0;
-  auto add = [&](int b0) {
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
       const bool ok = b0 + j * CB + tid < hi;
-      const unsigned b = __float_as_uint(v[j]);
-      const u64 f = fx40(v[j]);
-      gt += ok && (!filter || b > tau) ? f : 0ull;
-      ties += ok && filter && b == tau ? 1ull : 0ull;
+      if (ok && (b & mask) == prefix) {
+        atomicAdd(&hist[w][(b >> shift) & 255u], fx40(v[j]));
+        if constexpr (LAST) atomicAdd(&cnt[w][b & 255u], 1u);
+      }
+      if constexpr (LAST) above += ok && b > (prefix | 255u) ? fx40(v[j]) : 0ull;  // 24-bit prefix above
     }
   };
   add(lo);
@@ -403,22 +380,50 @@ __global__ __launch_bounds__(CB) void k_chunk_kept(const float* __restrict__ esc
     load_batch(e_row, b0, hi, v);
     add(b0);
   }
-  gt = wave_sum_u64(gt);
-  ties = wave_sum_u64(ties);
-  if ((tid & 63) == 0) { r1[w] = gt; r2[w] = ties; }
   __syncthreads();
-  if (tid == 0) {
-    u64 a = 0, b = 0;
-    for (int j = 0; j < CW; ++j) { a += r1[j]; b += r2[j]; }
-    cgt[(size_t)row * nc + c] = a;
-    cties[(size_t)row * nc + c] = b;
+  if constexpr (!LAST) {
+    add_row_bins(hist, rh + level * 256);
+  } else {
+    // thread t holds digit t: its mass (added into the row's histogram) and count, then the chunk's
+    // suffix sums over digits (within each wave by a scan, then the totals of the waves above)
+    u64 t = 0;
+    unsigned n = 0;
+#pragma unroll
+    for (int j = 0; j < CW; ++j) {
+      t += hist[j][tid];
+      n += cnt[j][tid];
+    }
+    if (t) atomicAdd(rh + level * 256 + tid, t);
+    const u64 incl = wave_incl_scan_dpp(t);
+    const u64 wtot = readlane_u64(incl, 63);
+    above = wave_sum_u64(above);
+    __syncthreads();  // every wave has read hist; reuse it for the wave totals and the above masses
+    if (lane == 0) {
+      hist[0][w] = wtot;
+      red[w] = above;
+    }
+    __syncthreads();
+    u64 suf = wtot - incl + t;
+#pragma unroll
+    for (int j = 0; j < CW; ++j)
+      if (j > w) suf += hist[0][j];
+    const size_t ci = (size_t)row * nc + c;
+    csuf[ci * 256 + tid] = suf;
+    ccnt[ci * 256 + tid] = n;
+    if (tid == 0) {
+      u64 a = 0;
+#pragma unroll
+      for (int j = 0; j < CW; ++j) a += red[j];
+      cabove[ci] = a;
+    }
   }
 }
 
 // the ordered draw: locate the crossing chunk from chunk totals, then walk that chunk only
 __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int V, int chunk, int nc, int filter,
-                                             const RowSel* __restrict__ sel, const u64* __restrict__ cgt,
-                                             const u64* __restrict__ cties, const u64* __restrict__ cmass,
+                                             float top_p, const u64* __restrict__ rowhist,
+                                             const u64* __restrict__ cabove, const u64* __restrict__ csuf,
+                                             const unsigned* __restrict__ ccnt, const u64* __restrict__ cmass,
                                              const float* __restrict__ u, int u_stride,
                                              const int32_t* __restrict__ col, int32_t* __restrict__ out,
                                              int out_stride) {
@@ -431,7 +436,10 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
   unsigned tau = 0;
   u64 ftau = 0, kties = 0, kept = 0;
   if (filter) {
-    const RowSel st = sel[row];
+    // tau and the kept ties from the row's four digit histograms (every wave selects the same integers)
+    u64 hb[kLevels][4];
+    load_row_bins(rowhist + (size_t)row * kLevels * 256, kLevels - 1, hb);
+    const RowSel st = select_above(hb, kLevels, top_p);
     tau = st.prefix;
     ftau = fx40(__uint_as_float(tau));
     kties = st.kties;
@@ -445,9 +453,14 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
       if (j < nc) kept += mv[j];
   }
   if (w == 0) {
-    // chunk scan in one wave (nc <= 64): kept mass per chunk = gt + its kept ties
-    const u64 gt = lane < nc ? cgt[(size_t)row * nc + lane] : 0;
-    const u64 ti = lane < nc ? cties[(size_t)row * nc + lane] : 0;
+    // chunk scan in one wave (nc <= 64): kept mass per chunk = gt + its kept ties, where gt is the mass of
+    // its values above tau (with filtering: above tau's 24-bit prefix, plus its digits above tau's digit;
+    // without: the whole chunk) and ti its values equal to tau
+    const size_t ci = (size_t)row * nc + min(lane, nc - 1);
+    const unsigned d = tau & 255u;
+    u64 gt = filter ? cabove[ci] + (d < 255u ? csuf[ci * 256 + d + 1] : 0ull) : cmass[ci];
+    u64 ti = filter ? (u64)ccnt[ci * 256 + d] : 0ull;
+    if (lane >= nc) gt = ti = 0;
     const u64 ties_incl = wave_incl_scan(ti, lane);
     const u64 ties_before = ties_incl - ti;
     const u64 kt = filter ? (kties > ties_before ? min(kties - ties_before, ti) : 0) : 0;
@@ -823,8 +836,8 @@ int sample_chunks(int V) {
 
 size_t sample_scratch_bytes(int S, int V) {
   const int nc = sample_chunks(V);
-  return (size_t)S * V * 4 + (size_t)S * nc * (4 + 4 + 8 * 3) + (size_t)S * kLevels * 256 * 8 +
-         (size_t)S * sizeof(RowSel) + 4096;
+  return (size_t)S * V * 4 + (size_t)S * nc * (4 + 4 + 8 + 8 + 256 * 8 + 256 * 4) + (size_t)S * kLevels * 256 * 8 +
+         4096;
 }
 
 int sample_rows_fitting(size_t bytes, int V) {
@@ -853,10 +866,10 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
   float* cmax = (float*)take((size_t)S * nc * 4);
   int* cidx = (int*)take((size_t)S * nc * 4);
   u64* cmass = (u64*)take((size_t)S * nc * 8);
-  u64* cgt = (u64*)take((size_t)S * nc * 8);
-  u64* cties = (u64*)take((size_t)S * nc * 8);
+  u64* cabove = (u64*)take((size_t)S * nc * 8);
+  u64* csuf = (u64*)take((size_t)S * nc * 256 * 8);
+  unsigned* ccnt = (unsigned*)take((size_t)S * nc * 256 * 4);
   u64* rowhist = (u64*)take((size_t)S * kLevels * 256 * 8);
-  RowSel* sel = (RowSel*)take((size_t)S * sizeof(RowSel));
   const dim3 rc(S, nc);
   if (temperature == 0.0f) {
     hipLaunchKernelGGL(k_chunk_argmax, rc, dim3(CB), 0, s, logits, V, chunk, cmax, cidx);
@@ -872,11 +885,15 @@ hipError_t launch_sample(hipStream_t s, const float* logits, int S, int V, float
   hipLaunchKernelGGL(k_chunk_max, rc, dim3(CB), 0, s, logits, V, chunk, cmax, rowhist);
   hipLaunchKernelGGL(k_chunk_exp, rc, dim3(CB), 0, s, logits, V, chunk, temperature, cmax, escr, cmass, rowhist,
                      filter);
-  if (filter)
-    for (int shift = 16; shift >= 0; shift -= 8)
-      hipLaunchKernelGGL(k_chunk_hist, rc, dim3(CB), 0, s, escr, V, chunk, shift, top_p, rowhist);
-  hipLaunchKernelGGL(k_chunk_kept, rc, dim3(CB), 0, s, escr, V, chunk, filter, top_p, rowhist, sel, cgt, cties);
-  hipLaunchKernelGGL(k_draw, dim3(S), dim3(RB), 0, s, escr, V, chunk, nc, filter, sel, cgt, cties, cmass, u,
+  if (filter) {
+    for (int shift = 16; shift >= 8; shift -= 8)
+      hipLaunchKernelGGL(k_chunk_hist<false>, rc, dim3(CB), 0, s, escr, V, chunk, shift, top_p, rowhist, nullptr,
+                         nullptr, nullptr);
+    hipLaunchKernelGGL(k_chunk_hist<true>, rc, dim3(CB), 0, s, escr, V, chunk, 0, top_p, rowhist, cabove, csuf,
+                       ccnt);
+  }
+  hipLaunchKernelGGL(k_draw, dim3(S), dim3(RB), 0, s, escr, V, chunk, nc, filter, top_p, rowhist, cabove, csuf, ccnt,
+                     cmass, u,
                      u_stride, col, out, out_stride);
   return hipGetLastError();
 }

@@ -46,10 +46,11 @@ def test_noalloc_draw_equals_rollout_sample_twice_the_second_smaller(V, T, top_p
 
 @pytest.mark.gpu
 def test_noalloc_draw_in_several_batches_of_the_fixed_scratch():
-    # 152064 logits per row (38 chunks): exp values, five words per chunk and four 256-bin digit histograms
-    # per row -- the 64 MiB scratch holds 108 rows, so 200 rows take two batches
+    # 152064 logits per row (38 chunks): exp values; per chunk four words, its 256 digit suffix sums and
+    # counts; four 256-bin digit histograms per row -- the 64 MiB scratch holds 91 rows, so 200 rows take
+    # three batches
     V, S = 152064, 200
-    per_row = 4 * V + 38 * 32 + 4 * 256 * 8 + 56
+    per_row = 4 * V + 38 * (24 + 256 * 12) + 4 * 256 * 8
     assert (R.NOALLOC_SCRATCH_BYTES - 4096) // per_row < S
     print(f"noalloc sampler V={V}: {S} rows in batches", flush=True)
     got, want = _draw_both(V, S, 0.9, 0.95, 11)
@@ -91,11 +92,11 @@ def test_noalloc_draw_matches_the_oracle_at_vocabularies_no_context_has(V, T, to
 def test_noalloc_validates_before_any_device_work():
     # fake (never dereferenced) addresses: every error below is raised before the device is touched
     fake = 1 << 20
-    # the largest row the 64 MiB scratch holds: 16,773,618 exp values, 64 chunks of five words, four 256-bin
-    # histograms, the row's selection and 4 KiB of alignment slack; one logit more is rejected
+    # the largest row the 64 MiB scratch holds: 16,724,608 exp values, 64 chunks (four words, 256 suffix sums
+    # and 256 counts each), four 256-bin histograms and 4 KiB of alignment slack; one logit more is rejected
     with pytest.raises(R.RolloutError, match="ENOMEM"):
-        R.rollout_sample_noalloc(fake, 1, 16_773_619, 1.0, 1.0, fake, fake)
-    assert "16773619 logits" in R.rollout_last_error()
+        R.rollout_sample_noalloc(fake, 1, 16_724_609, 1.0, 1.0, fake, fake)
+    assert "16724609 logits" in R.rollout_last_error()
     with pytest.raises(R.RolloutError, match="ENOMEM"):
         R.rollout_sample_noalloc(fake, 1, 1 << 24, 1.0, 1.0, fake, fake)
     for args in ((0, 1, 1024, 1.0, 1.0, fake, fake), (fake, 0, 1024, 1.0, 1.0, fake, fake),
