@@ -74,16 +74,11 @@ __device__ __forceinline__ u64 fx40(float e) {
   return sh > -24 ? mant >> (-sh) : 0;
 }
 
-// max of a row's nc chunk maxima, every load in flight at once (indices clamped, surplus masked)
-__device__ __forceinline__ float row_max(const float* cm, int nc) {
-  float v[kMaxChunks];
-#pragma unroll
-  for (int j = 0; j < kMaxChunks; ++j) v[j] = cm[min(j, nc - 1)];
-  float m = -INFINITY;
-#pragma unroll
-  for (int j = 0; j < kMaxChunks; ++j)
-    if (j < nc) m = fmaxf(m, v[j]);
-  return m;
+// this lane's share of a row's nc (<= 64) chunk maxima: one vector load per lane (lanes past nc re-read the
+// last); wave_max of it is the row maximum.  Uniform addresses would become scalar loads, at most 15 in
+// flight, whose round trips would come before the chunk's own loads.
+__device__ __forceinline__ float row_max_part(const float* cm, int nc) {
+  return cm[min((int)(threadIdx.x & 63), nc - 1)];
 }
 
 // One batch of a chunk: thread t takes ids b + j * CB + t (j < kPer), all kPer loads in flight before
@@ -296,18 +291,24 @@ __global__ __launch_bounds__(CB) void k_chunk_exp(const float* __restrict__ logi
   __shared__ u64 hist[CW][256];
   __shared__ u64 red[CW];
   const int row = blockIdx.x, c = blockIdx.y, nc = gridDim.y, tid = threadIdx.x, w = tid >> 6;
-  const float m = row_max(cmax + (size_t)row * nc, nc) / T;  // max of fp32(z / T) (see k_chunk_max)
   const float* z = logits + (size_t)row * V;
   float* e_row = escr + (size_t)row * V;
   const int lo = c * chunk, hi = min(V, lo + chunk);
+  // the row's chunk maxima, then the chunk's first batch, then the wait for the maxima alone (the load
+  // counter retires in issue order, so the batch stays in flight)
+  const float mpart = row_max_part(cmax + (size_t)row * nc, nc);
+  __builtin_amdgcn_sched_barrier(0);
+  float v[kPer];
+  load_batch(z, lo, hi, v);
+  __builtin_amdgcn_sched_barrier(0);
+  const float m = wave_max(mpart) / T;  // max of fp32(z / T) (see k_chunk_max)
   if (filter) {
     for (int i = tid; i < CW * 256; i += CB) (&hist[0][0])[i] = 0;
     __syncthreads();
   }
   u64 mass = 0;
   for (int b = lo; b < hi; b += kBatch) {
-    float v[kPer];
-    load_batch(z, b, hi, v);
+    if (b > lo) load_batch(z, b, hi, v);
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int i = b + j * CB + tid;
@@ -445,12 +446,9 @@ __global__ __launch_bounds__(RB) void k_draw(const float* __restrict__ escr, int
     kties = st.kties;
     kept = st.kept;
   } else {
-    u64 mv[kMaxChunks];
-#pragma unroll
-    for (int j = 0; j < kMaxChunks; ++j) mv[j] = cmass[(size_t)row * nc + min(j, nc - 1)];
-#pragma unroll
-    for (int j = 0; j < kMaxChunks; ++j)
-      if (j < nc) kept += mv[j];
+    // the row's total mass: one chunk per lane (nc <= 64), then a wave sum
+    const u64 cm = cmass[(size_t)row * nc + min(lane, nc - 1)];
+    kept = wave_sum_u64(lane < nc ? cm : 0ull);
   }
   if (w == 0) {
     // chunk scan in one wave (nc <= 64): kept mass per chunk = gt + its kept ties, where gt is the mass of
