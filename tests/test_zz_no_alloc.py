@@ -1,8 +1,8 @@
 """rollout_sample_noalloc, the allocation-free draw: the same tokens as rollout_sample, the entry point it is a
 variant of, on the same logits and uniforms -- bit for bit (both decide in exact integers) -- on two calls in
 a row, the second with fewer rows; rows beyond one batch of the fixed scratch; vocabularies that no context
-can have (not a multiple of 16), against the oracle; and argument validation that happens before any device
-work."""
+can have (not a multiple of 16) and the largest one the scratch holds, against the oracle; and argument
+validation that happens before any device work."""
 import numpy as np
 import pytest
 
@@ -87,6 +87,41 @@ def test_noalloc_draw_matches_the_oracle_at_vocabularies_no_context_has(V, T, to
         assert got[s] == tok, f"row {s}: gpu {got[s]} oracle {tok} margin {margin}"
         checked += 1
     assert checked >= S - 8
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("T,top_p", [(0.9, 0.95), (1.0, 1.0)])
+def test_noalloc_draw_at_the_largest_vocabulary_the_scratch_holds(T, top_p):
+    # 16,724,608 ids: 64 chunks of 64 batches each, one row per batch of the fixed scratch.  A thousand ids per
+    # row stand far above the rest, so the kept set and the draw land among them with CDF buckets of about
+    # 1e-3 of the mass (the oracle's margins are then far from the 1e-6 guard), while every pass still covers
+    # the whole row.
+    from oracle import sample_row
+
+    V, S = 16_724_608, 2
+    rng = np.random.default_rng(17)
+    z = rng.standard_normal((S, V), dtype=np.float32)
+    for s in range(S):
+        ids = rng.choice(V, 1000, replace=False)
+        z[s, ids] = 14.0 + rng.standard_normal(1000).astype(np.float32)
+    u = W.uniforms(S, 1, seed=19)[:, 0]
+    print(f"noalloc sampler at the largest vocabulary V={V} T={T} top_p={top_p}: {S} rows", flush=True)
+    dev = "cuda:0"
+    got = torch.full((S,), -1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream(device=dev)
+    R.rollout_sample_noalloc(torch.from_numpy(z).to(dev), S, V, T, top_p, torch.from_numpy(u).to(dev), got,
+                             stream.cuda_stream)
+    stream.synchronize()
+    got = got.cpu().numpy()
+    assert np.all((got >= 0) & (got < V))
+    checked = 0
+    for s in range(S):
+        tok, margin = sample_row(z[s], T, top_p, float(u[s]))
+        if margin < 1e-6:
+            continue
+        assert got[s] == tok, f"row {s}: gpu {got[s]} oracle {tok} margin {margin}"
+        checked += 1
+    assert checked >= 1
 
 
 def test_noalloc_validates_before_any_device_work():
