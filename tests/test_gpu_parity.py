@@ -301,6 +301,36 @@ def test_bf16_gqa7_teacher_forced_logits(blk, n_prompts, G, P, shared, waves, mo
     eng.close()
 
 
+@pytest.mark.parametrize("shared", ["0", "2"])
+def test_bf16_gqa7_context_beyond_4096_tokens_teacher_forced(shared, monkeypatch):
+    # A context of more than 256 blocks of 16 (4,096 tokens): the decode attention's workgroup of 256
+    # threads then copies the sequence's block table in more than one pass, and the prefill attention reads
+    # a 4,090-token prompt.  The decode steps cross from 256 to 257 blocks; with the shared-prefix path the
+    # prompt's 255 full blocks go to the prefix pass and the suffix pass starts at block 255.
+    set_attn_knobs(monkeypatch, shared, None)
+    n_prompts, G, P, N = 1, 2, 4090, 12
+    log(f"bf16 GQA 14/2 x 128 teacher forced, context {P} .. {P + N - 1} (beyond 256 blocks), shared={shared}")
+    S = n_prompts * G
+    cfg = R.model_config(GQA7_BF16, R.DTYPE_BF16, P, N, S)
+    eng = R.Engine(cfg, group_size=G)
+    model = OracleModel(shape_of(cfg), mode="bf16")
+    prompts = W.prompts(n_prompts, P, cfg.vocab, seed=45)
+    u = W.uniforms(S, N, seed=46)
+    ref = rollout(model, prompts, G, N, 1.0, 1.0, u)
+    log("  oracle done")
+    logits = torch.empty((S, cfg.vocab), dtype=torch.float32, device="cuda:0")
+    R.rollout_prefill(eng.ctx, to_dev(prompts, torch), n_prompts, P, G, logits)
+    eng.synchronize()
+    err = [float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][0])))]
+    for t in range(1, N):
+        R.rollout_decode_step(eng.ctx, to_dev(ref["tokens"][:, t - 1], torch), logits)
+        eng.synchronize()
+        err.append(float(np.max(np.abs(logits.cpu().numpy() - ref["logits"][t]))))
+    log(f"  max abs logit error per step: {[round(e, 5) for e in err]}")
+    assert max(err) <= 3e-2
+    eng.close()
+
+
 def test_bf16_gqa7_large_batch_teacher_forced_logits(monkeypatch):
     # 32 groups of 8: 512 (row, KV head) attention workgroups, where the library picks four waves by itself;
     # G x shared prompt = 8 x 64 keeps the shared-prefix pass off by size, so it is forced on here as well
